@@ -1,0 +1,335 @@
+"""Seeded synthetic inputs for sparse absorbed-MLA partial attention.
+
+This module only draws inputs.  It holds none of the attention arithmetic
+and is shared by the GPU path's tests and benchmark and by the oracle's
+tests, so both sides always consume the same bit patterns.
+
+Shapes follow a DeepSeek-V3-class absorbed MLA layer: per head a 512-wide
+latent part and a 64-wide decoupled-RoPE part (d_qk = 576, d_v = 512, the
+dimensions of the paper's wire format, Section 3.2), 64-token cache blocks,
+and a selection budget of 32 blocks = 2048 tokens, the V3.2 / GLM-5.1
+top-2048 budget the paper's Section 5.4 names.
+
+Recipe (all draws are PCG64 streams keyed by (seed, tensor tag, group), so a
+tensor is the same whatever the thread count):
+  * normals are float32 standard normals times sigma, rounded to bf16 by
+    round-to-nearest-even;
+  * a job's selection is drawn without replacement and sorted ascending;
+  * the pool is scattered: logical block -> pool block goes through a
+    seeded permutation of the pool;
+  * fp8 caches are the same values quantised per 64-token block and per
+    tensor (ckv, kpe separately) to OCP E4M3FN with scale absmax / 448,
+    round-to-nearest-even, saturating at +-448 (absmax 0 gives scale 1).
+"""
+from __future__ import annotations
+
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field
+
+import numpy as np
+
+DLAT = 512
+DPE = 64
+BLOCK = 64
+SCALE = 1.0 / math.sqrt(192.0)  # 1/sqrt(128 + 64), the softmax scale of every config
+
+# tensor tags of the PCG64 streams
+_T_QLAT, _T_QPE, _T_CKV, _T_KPE, _T_CHUNK, _T_SEL, _T_PERM, _T_TABLE = range(1, 9)
+_GROUP = 1 << 22  # elements per independent stream group
+
+
+def _threads():
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:
+        return 4
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns, round to nearest, ties to even."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> float32 (exact)."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(
+        np.float32)
+
+
+def normal_bf16(seed: int, tag: int, shape, sigma: float) -> np.ndarray:
+    """bf16 bits of sigma * N(0, 1), drawn in independent stream groups."""
+    n = int(np.prod(shape, dtype=np.int64))
+    out = np.empty(n, np.uint16)
+    groups = (n + _GROUP - 1) // _GROUP
+
+    def work(g):
+        lo = g * _GROUP
+        hi = min(n, lo + _GROUP)
+        rng = np.random.default_rng([seed, tag, g])
+        x = rng.standard_normal(hi - lo, dtype=np.float32)
+        if sigma != 1.0:
+            x *= np.float32(sigma)
+        out[lo:hi] = f32_to_bf16_bits(x)
+
+    if groups <= 1:
+        for g in range(groups):
+            work(g)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(work, range(groups)))
+    return out.reshape(shape)
+
+
+# ---------------------------------------------------------------- fp8 E4M3FN
+E4M3_MAX = 448.0
+
+
+def quantize_e4m3fn(y: np.ndarray) -> np.ndarray:
+    """float64 values -> OCP E4M3FN codes, round-to-nearest-even, saturating.
+
+    E4M3FN: bias 7, normal exponents -6..8, 3 mantissa bits, subnormals
+    m * 2^-9, largest finite 448 (code 0x7E), no infinities.
+    """
+    y = np.asarray(y, dtype=np.float64)
+    sign = np.signbit(y).astype(np.uint8) << np.uint8(7)
+    a = np.minimum(np.abs(y), E4M3_MAX)
+    # exponent of the binade of a, at least the smallest normal exponent -6
+    _, ex = np.frexp(a)  # a = f * 2^ex, f in [0.5, 1)
+    e = np.maximum(ex - 1, -6)
+    quantum = np.ldexp(1.0, e - 3)
+    q = np.rint(a / quantum) * quantum  # rint: ties to even
+    q = np.minimum(q, E4M3_MAX)
+    # encode q
+    _, ex2 = np.frexp(q)
+    e2 = ex2 - 1
+    normal = q >= 2.0 ** -6
+    e_field = np.where(normal, e2 + 7, 0)
+    m_norm = np.where(normal, np.ldexp(q, -e2) * 8.0 - 8.0, 0.0)
+    m_sub = np.where(normal, 0.0, q * 512.0)
+    m_field = np.where(normal, m_norm, m_sub)
+    code = (e_field.astype(np.int64) << 3) | np.rint(m_field).astype(np.int64)
+    return (code.astype(np.uint8) | sign).astype(np.uint8)
+
+
+def quantize_blocks_e4m3fn(bits: np.ndarray):
+    """Per-block fp8 quantisation of a bf16 pool [P, 64, D].
+
+    Returns (codes uint8 [P, 64, D], scales float32 [P]) with
+    scale = float32(absmax / 448) (1 when absmax is 0) and
+    code = E4M3FN(value / scale).
+    """
+    P = bits.shape[0]
+    codes = np.empty(bits.shape, np.uint8)
+    scales = np.empty(P, np.float32)
+    step = 256
+
+    def work(lo):
+        hi = min(P, lo + step)
+        x = bf16_bits_to_f32(bits[lo:hi])
+        amax = np.abs(x).reshape(hi - lo, -1).max(axis=1)
+        s = (amax / np.float32(E4M3_MAX)).astype(np.float32)
+        s[amax == 0] = np.float32(1.0)
+        scales[lo:hi] = s
+        codes[lo:hi] = quantize_e4m3fn(x.astype(np.float64) / s.astype(np.float64)[:, None, None])
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(work, range(0, P, step)))
+    return codes, scales
+
+
+# ------------------------------------------------------------------ workloads
+@dataclass
+class Workload:
+    """One call's inputs as host arrays (bf16 as uint16 bits)."""
+    name: str
+    q_lat: np.ndarray            # uint16 [R, Mq, H, 512]
+    q_pe: np.ndarray             # uint16 [R, Mq, H, 64]
+    ckv: np.ndarray              # uint16 [P, 64, 512] (or uint8 codes)
+    kpe: np.ndarray              # uint16 [P, 64, 64]  (or uint8 codes)
+    table: np.ndarray            # int32  [R, NB]
+    sel: np.ndarray              # int32  [R, K]
+    scale: float = SCALE
+    ckv_scale: np.ndarray | None = None  # float32 [P] for fp8 pools
+    kpe_scale: np.ndarray | None = None
+    n_requests: int = 0          # routed requests the call serves
+    merge_parts: int = 1         # partials merged per request (slot-major jobs)
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def shape(self):
+        R, Mq, H, _ = self.q_lat.shape
+        return dict(R=R, Mq=Mq, H=H, P=self.ckv.shape[0], NB=self.table.shape[1],
+                    K=self.sel.shape[1])
+
+    @property
+    def fp8(self):
+        return self.ckv.dtype == np.uint8
+
+    def n_selected_blocks(self):
+        return int((self.sel >= 0).sum())
+
+    def algorithmic_flops(self):
+        R, Mq, H, _ = self.q_lat.shape
+        per_job = (self.sel >= 0).sum(axis=1).astype(np.int64) * BLOCK
+        return int((per_job * Mq * H).sum()) * 2 * (DLAT + DPE + DLAT)
+
+    def kv_bytes(self):
+        per_tok = (DLAT + DPE) * (1 if self.fp8 else 2)
+        b = self.n_selected_blocks() * BLOCK * per_tok
+        if self.fp8:
+            b += self.n_selected_blocks() * 8  # two fp32 scales per block
+        return b
+
+    def to_fp8(self):
+        """The same values with E4M3FN caches (per-block absmax/448 scales)."""
+        ckv, cs = quantize_blocks_e4m3fn(self.ckv)
+        kpe, ks = quantize_blocks_e4m3fn(self.kpe)
+        return Workload(self.name + "-fp8", self.q_lat, self.q_pe, ckv, kpe, self.table,
+                        self.sel, self.scale, cs, ks, self.n_requests, self.merge_parts,
+                        dict(self.meta))
+
+
+def _perm(seed, n):
+    return np.random.default_rng([seed, _T_PERM]).permutation(n).astype(np.int32)
+
+
+def _queries(seed, R, Mq, H, sigma=1.0):
+    return (normal_bf16(seed, _T_QLAT, (R, Mq, H, DLAT), sigma),
+            normal_bf16(seed, _T_QPE, (R, Mq, H, DPE), sigma))
+
+
+def _pool(seed, P, sigma):
+    return (normal_bf16(seed, _T_CKV, (P, BLOCK, DLAT), sigma),
+            normal_bf16(seed, _T_KPE, (P, BLOCK, DPE), sigma))
+
+
+def tiny(seed=1):
+    """1 request, Mq=1, 16 heads, one 256-token chunk (4 blocks), all N(0,1);
+    2 of the 4 blocks selected by seed, 2 empty slots."""
+    q_lat, q_pe = _queries(seed, 1, 1, 16)
+    ckv, kpe = _pool(seed, 4, 1.0)
+    table = _perm(seed, 4)[None, :]
+    ids = np.sort(np.random.default_rng([seed, _T_SEL]).choice(4, 2, replace=False))
+    sel = np.array([[ids[0], ids[1], -1, -1]], np.int32)
+    return Workload("tiny", q_lat, q_pe, ckv, kpe, table.astype(np.int32), sel,
+                    n_requests=1, merge_parts=1)
+
+
+def dsv3_one_request(seed=2):
+    """Mq=1, 128 heads, q ~ N(0,1); one 4096-token chunk (64 blocks) ~ N(0,0.5);
+    top-32 blocks uniform without replacement."""
+    q_lat, q_pe = _queries(seed, 1, 1, 128)
+    ckv, kpe = _pool(seed, 64, 0.5)
+    table = _perm(seed, 64)[None, :]
+    sel = np.sort(np.random.default_rng([seed, _T_SEL]).choice(64, 32, replace=False))
+    return Workload("dsv3-one-request", q_lat, q_pe, ckv, kpe, table.astype(np.int32),
+                    sel[None, :].astype(np.int32), n_requests=1, merge_parts=1)
+
+
+def batched_merge(seed=3, n_requests=64, n_chunks=256, chunk_blocks=128, hits=4, topk=32):
+    """64 requests, Mq=1, 128 heads, q ~ N(0,1); a pool of 256 chunks x 8192
+    tokens ~ N(0,0.5); each request hits 4 distinct chunks and selects 32
+    blocks per chunk.  Jobs are slot-major (job = hit * n_requests + request),
+    so the partials of hit j of every request form one contiguous range for
+    the merge."""
+    q_req_lat, q_req_pe = _queries(seed, n_requests, 1, 128)
+    P = n_chunks * chunk_blocks
+    ckv, kpe = _pool(seed, P, 0.5)
+    perm = _perm(seed, P).reshape(n_chunks, chunk_blocks)
+    rng_c = np.random.default_rng([seed, _T_CHUNK])
+    chunks = np.stack([rng_c.choice(n_chunks, hits, replace=False) for _ in range(n_requests)])
+    rng_s = np.random.default_rng([seed, _T_SEL])
+    R = hits * n_requests
+    table = np.empty((R, chunk_blocks), np.int32)
+    sel = np.empty((R, topk), np.int32)
+    for j in range(hits):
+        for b in range(n_requests):
+            r = j * n_requests + b
+            table[r] = perm[chunks[b, j]]
+            sel[r] = np.sort(rng_s.choice(chunk_blocks, topk, replace=False))
+    q_lat = np.ascontiguousarray(np.broadcast_to(q_req_lat[None], (hits,) + q_req_lat.shape)
+                                 .reshape(R, 1, 128, DLAT))
+    q_pe = np.ascontiguousarray(np.broadcast_to(q_req_pe[None], (hits,) + q_req_pe.shape)
+                                .reshape(R, 1, 128, DPE))
+    return Workload("batched-merge", q_lat, q_pe, ckv, kpe, table, sel,
+                    n_requests=n_requests, merge_parts=hits,
+                    meta=dict(chunks=chunks))
+
+
+def zipf_ids(rng, n, k, a=1.1):
+    """k distinct positions in [0, n) by successive Zipf(a)-weighted draws
+    without replacement, sorted."""
+    w = (np.arange(1, n + 1, dtype=np.float64)) ** (-a)
+    return np.sort(rng.choice(n, k, replace=False, p=w / w.sum()))
+
+
+def few_head(seed=4, n_requests=16, mq=4, heads=16, chunk_blocks=512, topk=32):
+    """16 requests, Mq=4, 16 heads (one TP share of 128), q ~ N(0,1); each
+    request owns one 32768-token chunk (512 blocks) ~ N(0,1) and selects 32
+    blocks drawn Zipf(1.1) over block position; the 4 rows share it."""
+    q_lat, q_pe = _queries(seed, n_requests, mq, heads)
+    P = n_requests * chunk_blocks
+    ckv, kpe = _pool(seed, P, 1.0)
+    table = _perm(seed, P).reshape(n_requests, chunk_blocks)
+    rng_s = np.random.default_rng([seed, _T_SEL])
+    sel = np.stack([zipf_ids(rng_s, chunk_blocks, topk) for _ in range(n_requests)])
+    return Workload("few-head", q_lat, q_pe, ckv, kpe, table.astype(np.int32),
+                    sel.astype(np.int32), n_requests=n_requests, merge_parts=1)
+
+
+def dense_local(seed=5, n_requests=32, chunk_blocks=1024, fp8=False):
+    """32 requests, Mq=1, 128 heads, q ~ N(0,1); each attends all 1024 blocks
+    (65536 tokens) of its own chunk ~ N(0,0.5); optionally as an fp8 cache."""
+    q_lat, q_pe = _queries(seed, n_requests, 1, 128)
+    P = n_requests * chunk_blocks
+    ckv, kpe = _pool(seed, P, 0.5)
+    table = _perm(seed, P).reshape(n_requests, chunk_blocks)
+    sel = np.broadcast_to(np.arange(chunk_blocks, dtype=np.int32), (n_requests, chunk_blocks))
+    w = Workload("dense-local", q_lat, q_pe, ckv, kpe, table.astype(np.int32),
+                 np.ascontiguousarray(sel), n_requests=n_requests, merge_parts=1)
+    return w.to_fp8() if fp8 else w
+
+
+CONFIGS = {
+    "tiny": tiny,
+    "dsv3-one-request": dsv3_one_request,
+    "batched-merge": batched_merge,
+    "few-head": few_head,
+    "dense-local": dense_local,
+    "dense-local-fp8": lambda seed=5: dense_local(seed, fp8=True),
+}
+
+
+def make(name, seed=None, **kw):
+    fn = CONFIGS[name]
+    return fn(**kw) if seed is None else fn(seed=seed, **kw)
+
+
+def random_case(seed, R, Mq, H, P, NB, K, n_valid=None, sigma=1.0, allow_dup=False,
+                pad_pattern="tail"):
+    """Small random case for tests: R jobs over a P-block pool, NB logical
+    blocks per job, K slots of which n_valid[r] hold ids.  pad_pattern is
+    'tail' (ids first), 'interleaved' (empty slots spread) or 'none'."""
+    q_lat, q_pe = _queries(seed, R, Mq, H, sigma)
+    ckv, kpe = _pool(seed, P, sigma)
+    rng = np.random.default_rng([seed, _T_TABLE])
+    table = np.stack([rng.choice(P, NB, replace=NB > P) for _ in range(R)]).astype(np.int32)
+    rs = np.random.default_rng([seed, _T_SEL])
+    sel = np.full((R, K), -1, np.int32)
+    for r in range(R):
+        nv = K if n_valid is None else (n_valid[r] if np.ndim(n_valid) else n_valid)
+        if allow_dup:
+            ids = np.sort(rs.integers(0, NB, nv))
+        else:
+            ids = np.sort(rs.choice(NB, nv, replace=False))
+        if pad_pattern == "interleaved" and nv < K:
+            slots = np.sort(rs.choice(K, nv, replace=False))
+            sel[r, slots] = ids
+        else:
+            sel[r, :nv] = ids
+    return Workload(f"random-{seed}", q_lat, q_pe, ckv, kpe, table, sel,
+                    n_requests=R, merge_parts=1)
