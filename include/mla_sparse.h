@@ -1,0 +1,168 @@
+/*
+ * mla_sparse.h -- C ABI of libmla_sparse.so: sparse absorbed-MLA partial
+ * attention (the holder side of routing the query) and the log-sum-exp merge
+ * of partials (the requester side), on an AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Move the Query, Not the Cache" (arXiv 2606.01502).  A requester
+ * ships absorbed-MLA query rows, each d_qk = 576 wide (a 512-wide latent part
+ * and a 64-wide decoupled-RoPE part), to the instance holding a cached chunk;
+ * the holder attends them over the chunk's resident latent cache and returns a
+ * d_v = 512 wide partial output with the statistics that let the requester
+ * merge it exactly (Section 3.2, wire format).  Under sparse selection the
+ * holder attends only the entries the indexer selected, at their canonical
+ * positions (Sections 3.3, 5.4, 6.3).  The requester recombines partials by
+ * online softmax; the merge is commutative and has a zero-weight identity
+ * (Sections 2.2 and 3.3).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are passed as mla_tensor_t descriptors.  `data` is a DEVICE
+ *     pointer owned by the caller; the library never frees or keeps it past
+ *     the work it enqueues.  Descriptors and pointer arrays are read during
+ *     the call only and may be freed when it returns.
+ *   - Every call enqueues its kernels on `stream` (a hipStream_t; NULL is the
+ *     legacy default stream) and returns without synchronising.  Outputs are
+ *     valid once the stream reaches the enqueued work.  Inputs and outputs
+ *     must stay allocated until then.
+ *   - Calls return MLA_OK or a negative status.  Problems the host can see
+ *     (null pointers, dtypes, shapes, strides, alignment, aliasing) return
+ *     before anything is enqueued and write nothing; mla_last_error() then
+ *     describes the problem.  No C++ exception crosses the ABI.
+ *   - Device memory for split-K partials is allocated by the library on first
+ *     need and reused (one grow-only buffer per device and stream, freed at
+ *     unload).  Calls on different streams are independent; calls on one
+ *     stream are ordered by the stream.
+ */
+#ifndef MLA_SPARSE_H
+#define MLA_SPARSE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MLA_SPARSE_VERSION 1
+
+#define MLA_DLAT 512  /* latent width = d_v (Section 3.2)                    */
+#define MLA_DPE 64    /* decoupled-RoPE width = d_qk - d_v (Section 3.2)      */
+#define MLA_BLOCK 64  /* tokens per selectable cache block                   */
+#define MLA_MAX_PARTS 64
+
+typedef enum {
+  MLA_OK = 0,
+  MLA_ERR_INVALID_ARGUMENT = -1, /* null pointer, dtype, shape, stride, alignment, aliasing */
+  MLA_ERR_UNSUPPORTED = -2,      /* valid request this build does not implement       */
+  MLA_ERR_HIP = -3,              /* a HIP runtime call or a kernel launch failed      */
+  MLA_ERR_OUT_OF_MEMORY = -4     /* the split-K workspace could not be allocated      */
+} mla_status_t;
+
+typedef enum {
+  MLA_DTYPE_BF16 = 1,
+  MLA_DTYPE_FP8_E4M3FN = 2, /* OCP E4M3FN: bias 7, max 448, no infinities */
+  MLA_DTYPE_FP32 = 3,
+  MLA_DTYPE_INT32 = 4
+} mla_dtype_t;
+
+/* A strided view of device memory.  shape/stride beyond ndim are ignored;
+ * strides are in elements and the innermost stride must be 1. */
+typedef struct {
+  void* data;               /* device pointer, owned by the caller             */
+  int32_t dtype;            /* mla_dtype_t                                     */
+  int32_t ndim;             /* 1..4                                            */
+  int64_t shape[4];
+  int64_t stride[4];
+  const float* block_scale; /* fp8 cache pools only: device pointer to [P] fp32
+                               per-64-token-block scales (value = code * scale);
+                               must be NULL for every other tensor             */
+} mla_tensor_t;
+
+/*
+ * Sparse absorbed-MLA partial attention (the holder's partial, Sections 3.2,
+ * 3.3, 6.3).  R independent jobs (one per (request, chunk)); job r has
+ * Mq x H query rows that all share one selection of 64-token blocks.
+ *
+ *   q_lat             [R, Mq, H, 512] bf16   latent part of the absorbed query
+ *   q_pe              [R, Mq, H, 64]  bf16   decoupled-RoPE part (already rotated
+ *                                            by the requester; no rotation here)
+ *   ckv_pool          [P, 64, 512]    bf16 or fp8-e4m3fn (+block_scale), contiguous
+ *   kpe_pool          [P, 64, 64]     same dtype as ckv_pool, contiguous
+ *   chunk_block_table [R, NB] int32   logical block of job r's chunk -> pool block
+ *   sel_block_ids     [R, K]  int32   selected logical blocks; -1 marks an empty
+ *                                     slot; a block listed twice counts twice
+ *   scale                              multiplies q_lat.ckv + q_pe.kpe
+ *   out_lat           [R, Mq, H, 512] fp32   written: normalised partial output
+ *   out_lse           [R, Mq, H]      fp32   written: natural-log log-sum-exp
+ *
+ * For each row, with T the multiset of tokens of the selected blocks,
+ *   s_t = scale * (q_lat . ckv_t + q_pe . kpe_t),
+ *   out_lse = ln sum_T exp(s_t),   out_lat = sum_T exp(s_t - out_lse) * ckv_t,
+ * and for an empty T: out_lat = 0, out_lse = -inf.  No mask, no positions.
+ *
+ * Layout: q and out rows may be strided on the R, Mq and H dims (16-byte
+ * aligned rows); pools must be contiguous and 16-byte aligned.  Slot order
+ * does not change the result beyond rounding.  A selected id outside
+ * [0, NB), or a table entry outside [0, P), is a caller error that this call
+ * does not detect on the host: such a slot is skipped (treated as empty).
+ */
+mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                     const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                                     const mla_tensor_t* chunk_block_table,
+                                     const mla_tensor_t* sel_block_ids, float scale,
+                                     const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                                     void* stream);
+
+/* Tuning and test controls for mla_sparse_partial_attn_ex.  Zero fields mean
+ * "library's choice"; the result is the same up to rounding for any value. */
+typedef struct {
+  int32_t n_splits;    /* split-K: slot ranges per job, 1..K (0 = automatic) */
+  int32_t reserved[7]; /* must be zero                                        */
+} mla_partial_opts_t;
+
+/* mla_sparse_partial_attn with explicit options (opts may be NULL). */
+mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                        const mla_tensor_t* ckv_pool,
+                                        const mla_tensor_t* kpe_pool,
+                                        const mla_tensor_t* chunk_block_table,
+                                        const mla_tensor_t* sel_block_ids, float scale,
+                                        const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                                        const mla_partial_opts_t* opts, void* stream);
+
+/*
+ * Log-sum-exp merge of n_parts partials of the same rows (the requester's
+ * online-softmax recombination, Sections 2.2, 3.3 and 4.2).
+ *
+ *   out_lat[j]  [B, Mq, H, 512] fp32  normalised partial outputs, j < n_parts
+ *   out_lse[j]  [B, Mq, H]      fp32  their natural-log log-sum-exps
+ *   n_parts     1..MLA_MAX_PARTS
+ *   out         [B, Mq, H, 512] fp32  written
+ *
+ * Per row, over the live parts (lse != -inf): L = max lse_j,
+ * lse = L + ln sum exp(lse_j - L), out = sum exp(lse_j - lse) * out_lat[j].
+ * A part whose lse is -inf is skipped whatever its out_lat holds (even NaN);
+ * if no part is live the row is 0.  The parts may live anywhere but must
+ * share one set of strides; out may not overlap any input.
+ */
+mla_status_t mla_merge_partials(const mla_tensor_t* const* out_lat,
+                                const mla_tensor_t* const* out_lse, int32_t n_parts,
+                                const mla_tensor_t* out, void* stream);
+
+/* As mla_merge_partials, and also writes the merged log-sum-exp to
+ * merged_lse ([B, Mq, H] fp32, -inf for rows with no live part) unless it is
+ * NULL.  Merging merged partials again is exact (the merge is associative). */
+mla_status_t mla_merge_partials_ex(const mla_tensor_t* const* out_lat,
+                                   const mla_tensor_t* const* out_lse, int32_t n_parts,
+                                   const mla_tensor_t* out, const mla_tensor_t* merged_lse,
+                                   void* stream);
+
+/* Text describing the last non-OK status returned on the calling thread
+ * ("" if none).  Owned by the library; valid until the thread's next call. */
+const char* mla_last_error(void);
+
+/* MLA_SPARSE_VERSION of the loaded library. */
+int32_t mla_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLA_SPARSE_H */

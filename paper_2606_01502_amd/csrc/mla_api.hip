@@ -1,0 +1,373 @@
+// C ABI of libmla_sparse.so: argument validation, the split-K plan, the
+// split-K workspace and the kernel launches.  Declared in include/mla_sparse.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdint>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+
+#include "../../include/mla_sparse.h"
+#include "mla_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mla_status_t fail(mla_status_t st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+struct Extent {
+  uintptr_t lo, hi;  // [lo, hi) bytes touched
+};
+
+int dtype_size(int32_t dt) {
+  switch (dt) {
+    case MLA_DTYPE_BF16: return 2;
+    case MLA_DTYPE_FP8_E4M3FN: return 1;
+    case MLA_DTYPE_FP32: return 4;
+    case MLA_DTYPE_INT32: return 4;
+    default: return 0;
+  }
+}
+
+int64_t numel(const mla_tensor_t& t) {
+  int64_t n = 1;
+  for (int d = 0; d < t.ndim; ++d) n *= t.shape[d];
+  return n;
+}
+
+Extent extent(const mla_tensor_t& t) {
+  const int es = dtype_size(t.dtype);
+  if (numel(t) == 0) return {0, 0};
+  int64_t hi = 0;
+  for (int d = 0; d < t.ndim; ++d) hi += (t.shape[d] - 1) * t.stride[d];
+  const uintptr_t base = reinterpret_cast<uintptr_t>(t.data);
+  return {base, base + (uintptr_t)((hi + 1) * es)};
+}
+
+bool overlaps(const Extent& a, const Extent& b) {
+  if (a.lo == a.hi || b.lo == b.hi) return false;
+  return a.lo < b.hi && b.lo < a.hi;
+}
+
+// Common checks of one descriptor.  `name` is used in messages.
+mla_status_t check_tensor(const mla_tensor_t* t, const char* name, int32_t dtype, int ndim,
+                          bool allow_scale = false) {
+  if (!t) return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": null descriptor");
+  if (t->dtype != dtype)
+    return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": wrong dtype " + std::to_string(t->dtype));
+  if (t->ndim != ndim)
+    return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": expected " + std::to_string(ndim) +
+                                              " dims, got " + std::to_string(t->ndim));
+  for (int d = 0; d < ndim; ++d)
+    if (t->shape[d] < 0 || t->stride[d] < 0)
+      return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": negative shape or stride");
+  if (ndim > 0 && t->shape[ndim - 1] > 1 && t->stride[ndim - 1] != 1)
+    return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": innermost stride must be 1");
+  if (numel(*t) > 0 && !t->data)
+    return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": null data pointer");
+  if (!allow_scale && t->block_scale)
+    return fail(MLA_ERR_INVALID_ARGUMENT, std::string(name) + ": block_scale must be NULL");
+  return MLA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Rows of a [.., .., .., D] tensor are 16-byte aligned: base and every outer stride.
+bool rows_aligned(const mla_tensor_t& t, int es) {
+  if (!aligned16(t.data)) return false;
+  for (int d = 0; d + 1 < t.ndim; ++d)
+    if ((t.stride[d] * es) % 16 != 0) return false;
+  return true;
+}
+
+// Split-K workspace: one grow-only buffer per (device, stream).
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mutex;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(MLA_ERR_HIP, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  Workspace& ws = g_ws[{dev, stream}];
+  if (ws.bytes < bytes) {
+    if (ws.ptr) {
+      // the previous buffer may still be in use by work queued on this stream
+      if (hipStreamSynchronize(stream) != hipSuccess) return fail(MLA_ERR_HIP, "hipStreamSynchronize failed");
+      (void)hipFree(ws.ptr);
+      ws.ptr = nullptr;
+      ws.bytes = 0;
+    }
+    const size_t want = std::max(bytes, (size_t)1 << 20);
+    if (hipMalloc(&ws.ptr, want) != hipSuccess) {
+      (void)hipGetLastError();
+      ws.ptr = nullptr;
+      return fail(MLA_ERR_OUT_OF_MEMORY, "split-K workspace allocation of " + std::to_string(want) + " bytes failed");
+    }
+    ws.bytes = want;
+  }
+  *out = ws.ptr;
+  return MLA_OK;
+}
+
+int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mla_last_error(void) { return g_last_error.c_str(); }
+
+int32_t mla_version(void) { return MLA_SPARSE_VERSION; }
+
+mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                        const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                                        const mla_tensor_t* chunk_block_table,
+                                        const mla_tensor_t* sel_block_ids, float scale,
+                                        const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                                        const mla_partial_opts_t* opts, void* stream) {
+  try {
+    g_last_error.clear();
+    mla_status_t st;
+    if ((st = check_tensor(q_lat, "q_lat", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(q_pe, "q_pe", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if (!ckv_pool || !kpe_pool) return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool/kpe_pool: null descriptor");
+    const int32_t kv_dtype = ckv_pool->dtype;
+    if (kv_dtype != MLA_DTYPE_BF16 && kv_dtype != MLA_DTYPE_FP8_E4M3FN)
+      return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool: dtype must be bf16 or fp8-e4m3fn");
+    const bool fp8 = kv_dtype == MLA_DTYPE_FP8_E4M3FN;
+    if ((st = check_tensor(ckv_pool, "ckv_pool", kv_dtype, 3, fp8)) != MLA_OK) return st;
+    if ((st = check_tensor(kpe_pool, "kpe_pool", kv_dtype, 3, fp8)) != MLA_OK) return st;
+    if (fp8 && (!ckv_pool->block_scale || !kpe_pool->block_scale))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "fp8 pools need block_scale");
+    if ((st = check_tensor(chunk_block_table, "chunk_block_table", MLA_DTYPE_INT32, 2)) != MLA_OK) return st;
+    if ((st = check_tensor(sel_block_ids, "sel_block_ids", MLA_DTYPE_INT32, 2)) != MLA_OK) return st;
+    if ((st = check_tensor(out_lat, "out_lat", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
+    if (opts) {
+      for (int i = 0; i < 7; ++i)
+        if (opts->reserved[i]) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.reserved must be zero");
+      if (opts->n_splits < 0) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.n_splits must be >= 0");
+    }
+
+    const int64_t R = q_lat->shape[0], Mq = q_lat->shape[1], H = q_lat->shape[2];
+    const int64_t P = ckv_pool->shape[0];
+    const int64_t NB = chunk_block_table->shape[1], K = sel_block_ids->shape[1];
+    auto shape_is = [](const mla_tensor_t* t, std::initializer_list<int64_t> s) {
+      int d = 0;
+      for (int64_t v : s)
+        if (t->shape[d++] != v) return false;
+      return true;
+    };
+    if (q_lat->shape[3] != MLA_DLAT) return fail(MLA_ERR_INVALID_ARGUMENT, "q_lat: last dim must be 512");
+    if (!shape_is(q_pe, {R, Mq, H, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "q_pe: shape must be [R, Mq, H, 64]");
+    if (!shape_is(ckv_pool, {P, MLA_BLOCK, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool: shape must be [P, 64, 512]");
+    if (!shape_is(kpe_pool, {P, MLA_BLOCK, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "kpe_pool: shape must be [P, 64, 64] with the P of ckv_pool");
+    if (chunk_block_table->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_block_table: shape must be [R, NB]");
+    if (sel_block_ids->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K]");
+    if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
+    if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
+    if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||
+        kpe_pool->stride[0] != MLA_BLOCK * MLA_DPE || kpe_pool->stride[1] != MLA_DPE)
+      return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be contiguous");
+    if (!aligned16(ckv_pool->data) || !aligned16(kpe_pool->data))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be 16-byte aligned");
+    if (!rows_aligned(*q_lat, 2) || !rows_aligned(*q_pe, 2))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "q_lat/q_pe rows must be 16-byte aligned");
+    if (!rows_aligned(*out_lat, 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat rows must be 16-byte aligned");
+    if (!std::isfinite(scale)) return fail(MLA_ERR_INVALID_ARGUMENT, "scale must be finite");
+    if (R > INT32_MAX || Mq * H > (1 << 24) || K > INT32_MAX || NB > INT32_MAX || P > INT32_MAX)
+      return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the int32 index range");
+
+    const Extent outs[2] = {extent(*out_lat), extent(*out_lse)};
+    const Extent ins[7] = {extent(*q_lat), extent(*q_pe), extent(*ckv_pool), extent(*kpe_pool),
+                           extent(*chunk_block_table), extent(*sel_block_ids),
+                           {0, 0}};
+    if (overlaps(outs[0], outs[1])) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat and out_lse overlap");
+    for (const Extent& o : outs)
+      for (const Extent& i : ins)
+        if (overlaps(o, i)) return fail(MLA_ERR_INVALID_ARGUMENT, "an output overlaps an input");
+
+    const int64_t rows = Mq * H;
+    if (R == 0 || rows == 0) return MLA_OK;
+    if (fp8) return fail(MLA_ERR_UNSUPPORTED, "fp8-e4m3fn pools are not implemented in this build");
+
+    // ---- plan: row tiles of 128 rows (8 waves) or 64 rows (4 waves); split-K
+    // over slot ranges so that the grid covers the chip
+    const int waves = rows > 64 ? 8 : 4;
+    const int rows_wg = 16 * waves;
+    const int64_t row_tiles = (rows + rows_wg - 1) / rows_wg;
+    int64_t S;
+    if (opts && opts->n_splits > 0) {
+      S = std::min<int64_t>(opts->n_splits, std::max<int64_t>(K, 1));
+    } else {
+      const int64_t units = R * row_tiles;
+      S = std::max<int64_t>(1, (device_cus() + units - 1) / units);
+      S = std::min<int64_t>(S, std::max<int64_t>(K, 1));
+    }
+    S = std::max<int64_t>(S, (K + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
+    int64_t sps = std::max<int64_t>(1, (K + S - 1) / S);
+    S = std::max<int64_t>(1, (K + sps - 1) / sps);
+    if (R * row_tiles * S > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "grid too large");
+
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    mla::PartialParams p{};
+    p.q_lat = (const uint16_t*)q_lat->data;
+    p.q_pe = (const uint16_t*)q_pe->data;
+    p.ql_s0 = q_lat->stride[0]; p.ql_s1 = q_lat->stride[1]; p.ql_s2 = q_lat->stride[2];
+    p.qp_s0 = q_pe->stride[0]; p.qp_s1 = q_pe->stride[1]; p.qp_s2 = q_pe->stride[2];
+    p.ckv = (const uint8_t*)ckv_pool->data;
+    p.kpe = (const uint8_t*)kpe_pool->data;
+    p.ckv_scale = ckv_pool->block_scale;
+    p.kpe_scale = kpe_pool->block_scale;
+    p.table = (const int32_t*)chunk_block_table->data;
+    p.table_s0 = chunk_block_table->stride[0];
+    p.sel = (const int32_t*)sel_block_ids->data;
+    p.sel_s0 = sel_block_ids->stride[0];
+    p.P = P;
+    p.NB = (int32_t)NB;
+    p.K = (int32_t)K;
+    p.Mq = (int32_t)Mq;
+    p.H = (int32_t)H;
+    p.rows = (int32_t)rows;
+    p.n_splits = (int32_t)S;
+    p.slots_per_split = (int32_t)sps;
+    p.row_tiles = (int32_t)row_tiles;
+    p.scale_log2 = (float)((double)scale * 1.4426950408889634074);
+    p.out = (float*)out_lat->data;
+    p.out_s0 = out_lat->stride[0]; p.out_s1 = out_lat->stride[1]; p.out_s2 = out_lat->stride[2];
+    p.lse = (float*)out_lse->data;
+    p.lse_s0 = out_lse->stride[0]; p.lse_s1 = out_lse->stride[1]; p.lse_s2 = out_lse->stride[2];
+    if (S > 1) {
+      const size_t n_part_rows = (size_t)R * S * rows;
+      const size_t o_bytes = n_part_rows * MLA_DLAT * sizeof(float);
+      void* ws = nullptr;
+      if ((st = get_workspace(hs, o_bytes + n_part_rows * sizeof(float), &ws)) != MLA_OK) return st;
+      p.ws_o = (float*)ws;
+      p.ws_lse = (float*)((char*)ws + o_bytes);
+    }
+    hipError_t e = mla::launch_partial(p, (int)R, fp8, waves, hs);
+    if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
+    if (S > 1) {
+      mla::CombineParams c{};
+      c.ws_o = p.ws_o;
+      c.ws_lse = p.ws_lse;
+      c.R = (int32_t)R; c.S = (int32_t)S; c.Mq = (int32_t)Mq; c.H = (int32_t)H; c.rows = (int32_t)rows;
+      c.out = p.out; c.out_s0 = p.out_s0; c.out_s1 = p.out_s1; c.out_s2 = p.out_s2;
+      c.lse = p.lse; c.lse_s0 = p.lse_s0; c.lse_s1 = p.lse_s1; c.lse_s2 = p.lse_s2;
+      e = mla::launch_combine(c, hs);
+      if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("combine kernel launch: ") + hipGetErrorString(e));
+    }
+    return MLA_OK;
+  } catch (...) {
+    return fail(MLA_ERR_HIP, "internal error");
+  }
+}
+
+mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                     const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                                     const mla_tensor_t* chunk_block_table,
+                                     const mla_tensor_t* sel_block_ids, float scale,
+                                     const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                                     void* stream) {
+  return mla_sparse_partial_attn_ex(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
+                                    sel_block_ids, scale, out_lat, out_lse, nullptr, stream);
+}
+
+mla_status_t mla_merge_partials_ex(const mla_tensor_t* const* out_lat,
+                                   const mla_tensor_t* const* out_lse, int32_t n_parts,
+                                   const mla_tensor_t* out, const mla_tensor_t* merged_lse,
+                                   void* stream) {
+  try {
+    g_last_error.clear();
+    if (n_parts < 1 || n_parts > MLA_MAX_PARTS)
+      return fail(MLA_ERR_INVALID_ARGUMENT, "n_parts must be in 1.." + std::to_string(MLA_MAX_PARTS));
+    if (!out_lat || !out_lse) return fail(MLA_ERR_INVALID_ARGUMENT, "null part arrays");
+    mla_status_t st;
+    if ((st = check_tensor(out, "out", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
+    if (out->shape[3] != MLA_DLAT) return fail(MLA_ERR_INVALID_ARGUMENT, "out: last dim must be 512");
+    if (!rows_aligned(*out, 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "out rows must be 16-byte aligned");
+    if (merged_lse) {
+      if ((st = check_tensor(merged_lse, "merged_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
+      for (int d = 0; d < 3; ++d)
+        if (merged_lse->shape[d] != out->shape[d])
+          return fail(MLA_ERR_INVALID_ARGUMENT, "merged_lse: shape must be [B, Mq, H]");
+    }
+    mla::MergeParams p{};
+    std::string nm;
+    for (int j = 0; j < n_parts; ++j) {
+      nm = "out_lat[" + std::to_string(j) + "]";
+      if ((st = check_tensor(out_lat[j], nm.c_str(), MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
+      nm = "out_lse[" + std::to_string(j) + "]";
+      if ((st = check_tensor(out_lse[j], nm.c_str(), MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
+      for (int d = 0; d < 4; ++d)
+        if (out_lat[j]->shape[d] != out->shape[d])
+          return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat parts must have the shape of out");
+      for (int d = 0; d < 3; ++d)
+        if (out_lse[j]->shape[d] != out->shape[d])
+          return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse parts must be [B, Mq, H]");
+      for (int d = 0; d < 3; ++d)
+        if (out_lat[j]->stride[d] != out_lat[0]->stride[d] || out_lse[j]->stride[d] != out_lse[0]->stride[d])
+          return fail(MLA_ERR_UNSUPPORTED, "parts must share one set of strides");
+      if (!rows_aligned(*out_lat[j], 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "part rows must be 16-byte aligned");
+      const Extent eo = extent(*out);
+      if (overlaps(eo, extent(*out_lat[j])) || overlaps(eo, extent(*out_lse[j])))
+        return fail(MLA_ERR_INVALID_ARGUMENT, "out overlaps an input part");
+      if (merged_lse) {
+        const Extent el = extent(*merged_lse);
+        if (overlaps(el, extent(*out_lat[j])) || overlaps(el, extent(*out_lse[j])) || overlaps(el, eo))
+          return fail(MLA_ERR_INVALID_ARGUMENT, "merged_lse overlaps another tensor");
+      }
+      p.o[j] = (const float*)out_lat[j]->data;
+      p.lse[j] = (const float*)out_lse[j]->data;
+    }
+    const int64_t B = out->shape[0], Mq = out->shape[1], H = out->shape[2];
+    if (B * Mq * H > INT32_MAX / 2) return fail(MLA_ERR_UNSUPPORTED, "too many rows");
+    p.n_parts = n_parts;
+    p.B = (int32_t)B; p.Mq = (int32_t)Mq; p.H = (int32_t)H;
+    p.o_s0 = out_lat[0]->stride[0]; p.o_s1 = out_lat[0]->stride[1]; p.o_s2 = out_lat[0]->stride[2];
+    p.l_s0 = out_lse[0]->stride[0]; p.l_s1 = out_lse[0]->stride[1]; p.l_s2 = out_lse[0]->stride[2];
+    p.out = (float*)out->data;
+    p.out_s0 = out->stride[0]; p.out_s1 = out->stride[1]; p.out_s2 = out->stride[2];
+    if (merged_lse) {
+      p.out_lse = (float*)merged_lse->data;
+      p.ol_s0 = merged_lse->stride[0]; p.ol_s1 = merged_lse->stride[1]; p.ol_s2 = merged_lse->stride[2];
+    }
+    hipError_t e = mla::launch_merge(p, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("merge kernel launch: ") + hipGetErrorString(e));
+    return MLA_OK;
+  } catch (...) {
+    return fail(MLA_ERR_HIP, "internal error");
+  }
+}
+
+mla_status_t mla_merge_partials(const mla_tensor_t* const* out_lat,
+                                const mla_tensor_t* const* out_lse, int32_t n_parts,
+                                const mla_tensor_t* out, void* stream) {
+  return mla_merge_partials_ex(out_lat, out_lse, n_parts, out, nullptr, stream);
+}
+
+}  // extern "C"

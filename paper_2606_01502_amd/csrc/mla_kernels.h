@@ -1,0 +1,76 @@
+// Internal interface between the C-ABI host code and the HIP kernels of
+// libmla_sparse.so.  Not installed; the public interface is mla_sparse.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mla {
+
+constexpr int kDLat = 512;   // latent width (d_v)
+constexpr int kDPe = 64;     // decoupled-RoPE width
+constexpr int kBlock = 64;   // tokens per cache block
+constexpr int kThreads = 256;             // merge / combine workgroup size
+constexpr int kMaxSlotsPerSplit = 1024;   // selected-slot range one workgroup handles
+constexpr int kMaxParts = 64;
+
+// Partial attention over one (job, row tile, slot range) per workgroup.
+struct PartialParams {
+  const uint16_t* q_lat;  // bf16 bits
+  const uint16_t* q_pe;
+  int64_t ql_s0, ql_s1, ql_s2;  // element strides over (job, Mq, H)
+  int64_t qp_s0, qp_s1, qp_s2;
+  const uint8_t* ckv;  // pool base, bytes: [P][64][512] bf16 or e4m3 codes
+  const uint8_t* kpe;  // [P][64][64]
+  const float* ckv_scale;  // [P] (fp8 only)
+  const float* kpe_scale;
+  const int32_t* table;
+  int64_t table_s0;
+  const int32_t* sel;
+  int64_t sel_s0;
+  int64_t P;
+  int32_t NB, K;
+  int32_t Mq, H, rows;  // rows = Mq * H
+  int32_t n_splits, slots_per_split, row_tiles;
+  float scale_log2;  // softmax scale * log2(e)
+  // destination: direct (n_splits == 1) or split-K workspace
+  float* out;
+  int64_t out_s0, out_s1, out_s2;
+  float* lse;
+  int64_t lse_s0, lse_s1, lse_s2;
+  float* ws_o;    // [R][S][rows][512]
+  float* ws_lse;  // [R][S][rows]
+};
+
+// Combine of the S split partials of every job into the caller's outputs.
+struct CombineParams {
+  const float* ws_o;
+  const float* ws_lse;
+  int32_t R, S, Mq, H, rows;
+  float* out;
+  int64_t out_s0, out_s1, out_s2;
+  float* lse;
+  int64_t lse_s0, lse_s1, lse_s2;
+};
+
+// Merge of n parts given by pointers with shared strides.
+struct MergeParams {
+  const float* o[kMaxParts];
+  const float* lse[kMaxParts];
+  int32_t n_parts;
+  int32_t B, Mq, H;
+  int64_t o_s0, o_s1, o_s2;
+  int64_t l_s0, l_s1, l_s2;
+  float* out;
+  int64_t out_s0, out_s1, out_s2;
+  float* out_lse;  // may be null
+  int64_t ol_s0, ol_s1, ol_s2;
+};
+
+// Launchers; return hipSuccess or the launch error.
+// waves: 8 (row tiles of 128 rows) or 4 (row tiles of 64 rows)
+hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int waves, hipStream_t s);
+hipError_t launch_combine(const CombineParams& p, hipStream_t s);
+hipError_t launch_merge(const MergeParams& p, hipStream_t s);
+
+}  // namespace mla

@@ -1,0 +1,168 @@
+"""Python binding of libmla_sparse.so (C ABI in include/mla_sparse.h).
+
+Argument marshalling only: torch tensors are described to the library by
+pointer, dtype, shape and strides, and the current HIP stream is passed
+along.  Every step of the computation runs in the library's HIP kernels;
+there is no fallback, and a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmla_sparse.so")
+
+DLAT, DPE, BLOCK, MAX_PARTS = 512, 64, 64, 64
+
+MLA_OK = 0
+MLA_ERR_INVALID_ARGUMENT = -1
+MLA_ERR_UNSUPPORTED = -2
+MLA_ERR_HIP = -3
+MLA_ERR_OUT_OF_MEMORY = -4
+
+DTYPE_BF16, DTYPE_FP8_E4M3FN, DTYPE_FP32, DTYPE_INT32 = 1, 2, 3, 4
+
+EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex", "mla_merge_partials",
+           "mla_merge_partials_ex", "mla_last_error", "mla_version")
+
+
+class MlaError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+class Tensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4),
+                ("block_scale", ctypes.c_void_p)]
+
+
+class PartialOpts(ctypes.Structure):
+    _fields_ = [("n_splits", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the library (once) and declare its entry points."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(Tensor)
+    PP = ctypes.POINTER(P)
+    vp = ctypes.c_void_p
+    lib.mla_sparse_partial_attn.restype = ctypes.c_int
+    lib.mla_sparse_partial_attn.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P, vp]
+    lib.mla_sparse_partial_attn_ex.restype = ctypes.c_int
+    lib.mla_sparse_partial_attn_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P,
+                                               ctypes.POINTER(PartialOpts), vp]
+    lib.mla_merge_partials.restype = ctypes.c_int
+    lib.mla_merge_partials.argtypes = [PP, PP, ctypes.c_int32, P, vp]
+    lib.mla_merge_partials_ex.restype = ctypes.c_int
+    lib.mla_merge_partials_ex.argtypes = [PP, PP, ctypes.c_int32, P, P, vp]
+    lib.mla_last_error.restype = ctypes.c_char_p
+    lib.mla_last_error.argtypes = []
+    lib.mla_version.restype = ctypes.c_int32
+    lib.mla_version.argtypes = []
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+_TORCH_DTYPES = {
+    torch.bfloat16: DTYPE_BF16,
+    torch.float32: DTYPE_FP32,
+    torch.int32: DTYPE_INT32,
+    torch.uint8: DTYPE_FP8_E4M3FN,
+    torch.float8_e4m3fn: DTYPE_FP8_E4M3FN,
+}
+
+
+def describe(t: torch.Tensor | None, block_scale: torch.Tensor | None = None) -> Tensor | None:
+    """mla_tensor_t for a torch tensor (uint8 tensors are fp8-e4m3fn codes)."""
+    if t is None:
+        return None
+    if t.dim() > 4:
+        raise ValueError("at most 4 dims")
+    d = Tensor()
+    d.data = t.data_ptr() if t.numel() else None
+    d.dtype = _TORCH_DTYPES.get(t.dtype, 0)
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.stride[i] = t.stride(i)
+    if block_scale is not None:
+        if block_scale.dtype != torch.float32 or not block_scale.is_contiguous():
+            raise ValueError("block_scale must be contiguous float32")
+        d.block_scale = block_scale.data_ptr()
+    return d
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(lib, st):
+    if st != MLA_OK:
+        raise MlaError(st, lib.mla_last_error().decode())
+
+
+def _ref(d):
+    return ctypes.byref(d) if d is not None else None
+
+
+def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
+                        scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
+                        n_splits=0, stream=None):
+    """Partial attention of each job's Mq x H rows over its selected blocks.
+
+    Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
+    """
+    lib = load()
+    R, Mq, H, _ = q_lat.shape
+    if out_lat is None:
+        out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
+    if out_lse is None:
+        out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
+    opts = PartialOpts()
+    opts.n_splits = int(n_splits)
+    st = lib.mla_sparse_partial_attn_ex(
+        _ref(describe(q_lat)), _ref(describe(q_pe)), _ref(describe(ckv_pool, ckv_scale)),
+        _ref(describe(kpe_pool, kpe_scale)), _ref(describe(chunk_block_table)),
+        _ref(describe(sel_block_ids)), ctypes.c_float(scale), _ref(describe(out_lat)),
+        _ref(describe(out_lse)), ctypes.byref(opts), _stream(stream))
+    _check(lib, st)
+    return out_lat, out_lse
+
+
+def merge_partials(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
+    """LSE merge of partials (lists of [B, Mq, H, 512] / [B, Mq, H] fp32).
+
+    Returns out (and the merged lse when out_lse is given or requested by
+    passing out_lse=True)."""
+    lib = load()
+    n = len(parts_lat)
+    if n != len(parts_lse):
+        raise ValueError("parts_lat and parts_lse differ in length")
+    want_lse = out_lse is not None
+    if out is None:
+        out = torch.empty_like(parts_lat[0])
+    if out_lse is True:
+        out_lse = torch.empty_like(parts_lse[0])
+    d_lat = [describe(t) for t in parts_lat]
+    d_lse = [describe(t) for t in parts_lse]
+    arr_lat = (ctypes.POINTER(Tensor) * max(n, 1))(*[ctypes.pointer(d) for d in d_lat])
+    arr_lse = (ctypes.POINTER(Tensor) * max(n, 1))(*[ctypes.pointer(d) for d in d_lse])
+    st = lib.mla_merge_partials_ex(arr_lat, arr_lse, n, _ref(describe(out)),
+                                   _ref(describe(out_lse)) if want_lse else None, _stream(stream))
+    _check(lib, st)
+    return (out, out_lse) if want_lse else out

@@ -1,0 +1,142 @@
+"""HIP path against the oracle, element by element, through the C ABI.
+
+Small cases cover several tiles, ragged row counts, empty / padded /
+duplicated / invalid selections and every split-K setting; the workload
+configurations run at full size, compared on the rows the oracle can afford.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_01502_amd import workloads as W
+from tests import gpu_helpers as G
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle(w, jobs=None):
+    if jobs is None:
+        return oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                              w.ckv_scale, w.kpe_scale)
+    jobs = np.asarray(jobs)
+    return oracle.partial(w.q_lat[jobs], w.q_pe[jobs], w.ckv, w.kpe, w.table[jobs], w.sel[jobs],
+                          w.scale, w.ckv_scale, w.kpe_scale)
+
+
+def _check_case(w, n_splits=0, what=""):
+    t = G.upload(w)
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits)
+    ref_o, ref_l = _oracle(w)
+    return G.assert_parity(out, lse, ref_o, ref_l, what or w.name)
+
+
+def test_tiny_config():
+    print("case: tiny", flush=True)
+    _check_case(W.tiny())
+
+
+@pytest.mark.parametrize("n_splits", [0, 1, 2, 3, 7])
+def test_small_random_all_splits(n_splits):
+    print(f"case: random splits={n_splits}", flush=True)
+    w = W.random_case(101, R=3, Mq=1, H=16, P=20, NB=9, K=7)
+    _check_case(w, n_splits)
+
+
+@pytest.mark.parametrize("mq,h", [(1, 1), (3, 7), (1, 64), (2, 40), (1, 128), (2, 128), (5, 31)])
+def test_ragged_rows(mq, h):
+    """Row counts below, at and above the 64- and 128-row tiles."""
+    print(f"case: ragged mq={mq} h={h}", flush=True)
+    w = W.random_case(102 + mq * 1000 + h, R=2, Mq=mq, H=h, P=12, NB=6, K=3, sigma=0.7)
+    _check_case(w)
+
+
+def test_padding_duplicates_and_empty_jobs():
+    print("case: padding", flush=True)
+    w = W.random_case(103, R=4, Mq=1, H=32, P=10, NB=6, K=6, n_valid=[0, 1, 3, 6],
+                      allow_dup=True, pad_pattern="interleaved")
+    for s in (0, 1, 2, 6):
+        _check_case(w, s, f"padding splits={s}")
+
+
+def test_no_slots_at_all():
+    print("case: K=0", flush=True)
+    w = W.random_case(104, R=2, Mq=1, H=16, P=4, NB=4, K=1)
+    w.sel = np.zeros((2, 0), np.int32)
+    t = G.upload(w)
+    out, lse = G.run_partial(t, w.scale)
+    assert np.all(out == 0) and np.all(lse == -np.inf)
+
+
+def test_invalid_ids_are_skipped():
+    """Ids outside [0, NB) and table entries outside [0, P) count as empty
+    slots (the header's documented behaviour)."""
+    print("case: invalid ids", flush=True)
+    w = W.random_case(105, R=2, Mq=1, H=16, P=8, NB=5, K=4)
+    sel = w.sel.copy()
+    sel[0, 1] = 5          # >= NB
+    sel[1, 2] = -7         # negative, not -1
+    table = w.table.copy()
+    table[1, sel[1, 0]] = 8  # >= P
+    w_bad = W.Workload("bad", w.q_lat, w.q_pe, w.ckv, w.kpe, table, sel)
+    t = G.upload(w_bad)
+    out, lse = G.run_partial(t, w.scale)
+    clean = sel.copy()
+    clean[0, 1] = -1
+    clean[1, 2] = -1
+    clean[1, 0] = -1
+    ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, table, clean, w.scale)
+    G.assert_parity(out, lse, ref_o, ref_l, "invalid ids")
+
+
+def test_large_scale_near_one_hot():
+    print("case: one-hot", flush=True)
+    w = W.random_case(106, R=1, Mq=1, H=16, P=6, NB=4, K=4)
+    w.scale = 2.0
+    _check_case(w)
+
+
+def test_zero_query_gives_mean():
+    print("case: zero query", flush=True)
+    w = W.random_case(107, R=1, Mq=1, H=16, P=6, NB=4, K=3)
+    w.q_lat = np.zeros_like(w.q_lat)
+    w.q_pe = np.zeros_like(w.q_pe)
+    _check_case(w)
+
+
+def test_many_slots_split_limits():
+    """More slots than one workgroup compacts at once (1024) and long splits."""
+    print("case: many slots", flush=True)
+    w = W.random_case(108, R=1, Mq=1, H=16, P=1500, NB=1400, K=1300, sigma=0.5)
+    for s in (1, 2, 0):
+        _check_case(w, s, f"many slots splits={s}")
+
+
+def test_split_invariance_gpu_only():
+    """Different split plans agree with each other within rounding."""
+    print("case: split invariance", flush=True)
+    w = W.random_case(109, R=2, Mq=1, H=128, P=40, NB=33, K=32, sigma=0.5)
+    t = G.upload(w)
+    outs = [G.run_partial(t, w.scale, n_splits=s) for s in (1, 2, 4, 32)]
+    for o, l in outs[1:]:
+        assert np.abs(l - outs[0][1]).max() < 1e-4
+        assert G.row_errors(o, outs[0][0]).max() < 5e-3
+
+
+def test_deterministic_run_to_run():
+    print("case: determinism", flush=True)
+    w = W.random_case(110, R=3, Mq=1, H=128, P=40, NB=20, K=12, sigma=0.5)
+    t = G.upload(w)
+    a = G.run_partial(t, w.scale, n_splits=3)
+    b = G.run_partial(t, w.scale, n_splits=3)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_dsv3_one_request_config():
+    print("case: dsv3-one-request", flush=True)
+    _check_case(W.dsv3_one_request())
+
+
+def test_few_head_config_full():
+    print("case: few-head full", flush=True)
+    _check_case(W.few_head())
