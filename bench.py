@@ -1,0 +1,193 @@
+"""Benchmark of the hot path on one MI355X: sparse absorbed-MLA partial
+attention of routed query rows over selected 64-token latent blocks, then the
+requester-side LSE merge of the partials.
+
+One step = one pass of the whole path over one batch: mla_sparse_partial_attn
+over every (request, chunk) job, then mla_merge_partials over each request's
+partials.  Default workload: 64 routed requests (Mq = 1, 128 heads), each
+hitting 4 chunks of a 256-chunk x 8192-token bf16 pool and selecting 32
+blocks (2048 tokens) per chunk -> 256 partials merged into 64 outputs.
+
+Prints one JSON line.  `value` is microseconds per routed request (whole step
+/ requests, inputs resident in HBM); the dominant kernel's roofline uses
+algorithmic bytes (selected KV + query rows + partial outputs) over its
+HIP-event duration; `cpu_baseline` is the oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+DLAT, DPE, BLOCK = 512, 64, 64
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="batched-merge",
+                    help="batched-merge | dsv3-one-request | few-head | dense-local | "
+                         "dense-local-fp8 | tiny")
+    ap.add_argument("--n-splits", type=int, default=0, help="split-K override (0 = library)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample (0 = skip)")
+    return ap.parse_args()
+
+
+def algorithmic(w):
+    """(FLOP, bytes) of one partial-attention launch over workload w."""
+    R, Mq, H, _ = w.q_lat.shape
+    rows = R * Mq * H
+    nblk = int((w.sel >= 0).sum())
+    flops = w.algorithmic_flops()
+    kv = nblk * BLOCK * (DLAT + DPE) * (1 if w.fp8 else 2) + (nblk * 8 if w.fp8 else 0)
+    q = rows * (DLAT + DPE) * 2
+    out = rows * (DLAT + 1) * 4
+    return flops, kv + q + out, kv
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import oracle
+    from paper_2606_01502_amd import mla, workloads as W
+    from tests import gpu_helpers as G
+
+    mla.load()  # fail loudly before any work if the library is missing
+    w = W.make(args.workload)
+    R, Mq, H, _ = w.q_lat.shape
+    t = G.upload(w)
+    dev = G.device()
+    out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=dev)
+    out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=dev)
+    n_req = w.n_requests
+    parts = w.merge_parts
+    merged = torch.empty((n_req, Mq, H, DLAT), dtype=torch.float32, device=dev) if parts > 1 else None
+    part_lat = [out_lat[j * n_req:(j + 1) * n_req] for j in range(parts)]
+    part_lse = [out_lse[j * n_req:(j + 1) * n_req] for j in range(parts)]
+
+    def partial():
+        mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"], t["sel"],
+                                w.scale, out_lat, out_lse, t["ckv_scale"], t["kpe_scale"],
+                                n_splits=args.n_splits)
+
+    def merge():
+        if merged is not None:
+            mla.merge_partials(part_lat, part_lse, out=merged)
+
+    for _ in range(args.warmup):
+        partial()
+        merge()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        ev[k][0].record()
+        partial()
+        ev[k][1].record()
+        merge()
+        ev[k][2].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / K
+    partial_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]))
+    merge_ms = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]))
+
+    flops, alg_bytes, kv_bytes = algorithmic(w)
+    part_s = partial_ms * 1e-3
+    achieved = alg_bytes / part_s / 1e9
+    tflops = flops / part_s / 1e12
+    us_per_req = ms_step * 1e3 / n_req
+
+    # ---- oracle on a bounded sample of the same workload (whole requests)
+    cpu = None
+    parity = None
+    if args.cpu_seconds > 0:
+        out_np = out_lat.cpu().numpy()
+        lse_np = out_lse.cpu().numpy()
+        merged_np = merged.cpu().numpy() if merged is not None else None
+
+        def jobs_of(reqs):
+            # slot-major like the workload: hit j of every sampled request, then hit j+1
+            reqs = np.asarray(reqs)
+            return np.concatenate([j * n_req + reqs for j in range(parts)])
+
+        def run_oracle(reqs):
+            js = jobs_of(reqs)
+            return js, oracle.partial(w.q_lat[js], w.q_pe[js], w.ckv, w.kpe, w.table[js], w.sel[js],
+                                      w.scale, w.ckv_scale, w.kpe_scale)
+
+        ts = time.perf_counter()
+        js, (o1, l1) = run_oracle([0])
+        one = time.perf_counter() - ts
+        n = int(min(n_req, max(1, round(args.cpu_seconds / max(one, 1e-3)))))
+        reqs = list(range(n))
+        ts = time.perf_counter()
+        js, (o_ref, l_ref) = run_oracle(reqs)
+        if parts > 1:
+            po = np.stack([o_ref[j * n:(j + 1) * n] for j in range(parts)])
+            pl = np.stack([l_ref[j * n:(j + 1) * n] for j in range(parts)])
+            m_ref, _ = oracle.merge(po, pl)
+        elapsed = time.perf_counter() - ts
+        cpu = {"value": elapsed * 1e6 / n, "unit": "us/request", "cores": oracle.default_threads(),
+               "kind": "oracle",
+               "sample": f"{n} of {n_req} requests ({len(js)} of {R} partial jobs"
+                         f"{' + their merge' if parts > 1 else ''}), fp64 C oracle"}
+        rel = G.row_errors(out_np[js].astype(np.float64), o_ref)
+        lse_err = np.abs(lse_np[js] - l_ref)
+        parity = {"rows": int(rel.size), "max_row_rel_err": float(rel.max()),
+                  "max_lse_abs_err": float(lse_err[np.isfinite(l_ref)].max())
+                  if np.isfinite(l_ref).any() else 0.0}
+        if parts > 1:
+            parity["merge_max_row_rel_err"] = float(
+                G.row_errors(merged_np[:n].astype(np.float64), m_ref).max())
+
+    res = {
+        "metric": "us per routed request (sparse MLA partial attn + LSE merge)",
+        "value": us_per_req,
+        "unit": "us/request",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8-e4m3 kv, bf16 mfma" if w.fp8 else "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "requests": n_req, "jobs": R, "mq": Mq, "heads": H,
+                   "selected_blocks": int((w.sel >= 0).sum()), "block_tokens": BLOCK,
+                   "pool_blocks": int(w.ckv.shape[0]), "merge_parts": parts},
+        "tflops": tflops,
+        "pct_bf16_mfma_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
+        "partial_kernel_us": partial_ms * 1e3,
+        "merge_us": merge_ms * 1e3 if merged is not None else 0.0,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "partial_bf16_kernel", "algorithmic_bytes": alg_bytes,
+                     "kv_bytes": kv_bytes, "flops": flops},
+        "cpu_baseline": cpu,
+        "parity_sample": parity,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -215,10 +215,10 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (R == 0 || rows == 0) return MLA_OK;
     if (fp8) return fail(MLA_ERR_UNSUPPORTED, "fp8-e4m3fn pools are not implemented in this build");
 
-    // ---- plan: row tiles of 128 rows (8 waves) or 64 rows (4 waves); split-K
-    // over slot ranges so that the grid covers the chip
-    const int waves = rows > 64 ? 8 : 4;
-    const int rows_wg = 16 * waves;
+    // ---- plan: row tiles of 128 or 64 rows (4 waves of 32 or 16 rows);
+    // split-K over slot ranges so that the grid covers the chip
+    const int row_groups = rows > 64 ? 2 : 1;
+    const int rows_wg = 64 * row_groups;
     const int64_t row_tiles = (rows + rows_wg - 1) / rows_wg;
     int64_t S;
     if (opts && opts->n_splits > 0) {
@@ -269,7 +269,7 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       p.ws_o = (float*)ws;
       p.ws_lse = (float*)((char*)ws + o_bytes);
     }
-    hipError_t e = mla::launch_partial(p, (int)R, fp8, waves, hs);
+    hipError_t e = mla::launch_partial(p, (int)R, fp8, row_groups, hs);
     if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
     if (S > 1) {
       mla::CombineParams c{};

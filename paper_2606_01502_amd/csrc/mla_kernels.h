@@ -68,8 +68,8 @@ struct MergeParams {
 };
 
 // Launchers; return hipSuccess or the launch error.
-// waves: 8 (row tiles of 128 rows) or 4 (row tiles of 64 rows)
-hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int waves, hipStream_t s);
+// row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows)
+hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_merge(const MergeParams& p, hipStream_t s);
 

@@ -1,38 +1,37 @@
 // Sparse absorbed-MLA partial attention for gfx950 (MI355X).
 //
-// One workgroup (NW = 8 or 4 waves) handles one (job, row tile of 16*NW
-// rows, slot range).  The rows
+// One workgroup of 4 waves handles one (job, row tile, slot range).  The rows
 // of a job (Mq x H query rows; a row is a 512-wide latent part plus a 64-wide
 // decoupled-RoPE part, the paper's d_qk = 576 wire row of Section 3.2) share
 // one selection of 64-token cache blocks, so each selected block is read from
-// HBM once per workgroup and staged in LDS for all rows:
+// HBM once per workgroup and staged in LDS for all of its rows:
 //
 //   gather   direct-to-LDS 16-byte loads (global_load_lds_dwordx4) of each
-//            selected block, 32 tokens (36 KiB) at a time, into a ring of four
-//            LDS buffers; up to three half-blocks are in flight while one is
-//            computed.  The chunk's block table maps the selected logical
-//            block to its pool block.
-//   S^T      = K . Q^T per wave for its 16 rows: bf16 MFMA 16x16x32, K read
+//            selected block (64 KiB latent + 8 KiB RoPE rows) into one of two
+//            LDS buffers; block i+1 streams in while block i is computed.  The
+//            chunk's block table maps the selected logical block to its pool
+//            block; one workgroup barrier per block.
+//   S^T      = K . Q^T per wave for its 16*RG rows: bf16 MFMA 16x16x32, K read
 //            from LDS (b128), Q held in registers for the whole kernel.
 //   softmax  online, in the exp2 domain, with wavefront reductions; the
-//            running max is only moved when a block raises it by more than
-//            2^8, so the accumulator is rarely rescaled (exact either way).
-//   P        bf16 probabilities go through a small swizzled LDS tile so every
-//            wave sees all rows.
-//   O^T     += V^T . P^T per wave for its 512/NW latent columns and all rows
-//            of the tile: bf16 MFMA, V^T read with the transposing LDS read
-//            (ds_read_b64_tr_b16) from the same staged tile, since the value
-//            is the latent part of the key (Section 3.2).
+//            running max only moves when a block raises it by more than 2^8,
+//            so the accumulator is rarely rescaled (exact either way).
+//   O^T     += V^T . P^T per wave for its rows and all 512 latent columns:
+//            bf16 MFMA with P^T taken straight from the S^T accumulator layout
+//            (the k index of the product is a fixed permutation of the block's
+//            tokens) and V^T read with the transposing LDS read
+//            (ds_read_b64_tr_b16) from the same staged tile, since the value is
+//            the latent part of the key (Section 3.2).  O lives in the
+//            accumulation registers for the whole kernel.
 //   epilogue normalised output and lse = max + ln(sum) per row, either to the
 //            caller's buffers or, under split-K, to a workspace that the
 //            combine kernel reduces with the merge algebra (Section 3.3).
 //
-// LDS swizzles (token t within a half-block, 16-byte chunk c within a row):
-//   latent rows (1 KiB):   chunk c lives in slot c ^ ((t & 15) ^ ((t & 16) >> 2))
-//   RoPE rows (128 B):     chunk c lives in slot c ^ ((t >> 1) & 7)
-//   P rows (64 B):         chunk c lives in slot c ^ ((row >> 2) & 3)
-// so the b128 key reads, the transposing value reads and the P reads all hit
-// distinct banks at the minimum number of LDS cycles.
+// LDS swizzles (token t of the block, 16-byte chunk c of its row): latent
+// chunk c lives in slot c ^ (t & 15); RoPE chunk c in slot c ^ ((t >> 1) & 7).
+// The b128 key reads (16 consecutive tokens, one chunk) and the transposing
+// value reads (16 consecutive tokens, two chunks) then cover every LDS bank at
+// the minimum number of cycles.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -44,70 +43,152 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef int i32x2_t __attribute__((ext_vector_type(2)));
-typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
 
-constexpr int kNumBuf = 4;
-constexpr int kHalfTokens = 32;
-constexpr int kHalfCkvBytes = kHalfTokens * kDLat * 2;  // 32 KiB
-constexpr int kHalfKpeBytes = kHalfTokens * kDPe * 2;   // 4 KiB
-constexpr int kHalfBytes = kHalfCkvBytes + kHalfKpeBytes;
-constexpr int kLoadsPerHalf = 9;  // per wave: 8 latent rows + 1 KiB of RoPE rows
-constexpr float kTau = 8.0f;      // lazy-rescale threshold, log2 units
+constexpr int kCkvBytes = kBlock * kDLat * 2;           // 64 KiB of latent rows
+constexpr int kBufBytes = kCkvBytes + kBlock * kDPe * 2;  // + 8 KiB of RoPE rows
+constexpr int kLoadsPerBlock = 18;  // per wave: 16 latent rows + 2 KiB of RoPE rows
+constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
 
 // s_waitcnt immediate (gfx9 encoding) that waits for vmcnt <= n only.
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-template <int NW>
 struct Lds {
-  static constexpr int kRowsWg = 16 * NW;
-  static constexpr int kP = kNumBuf * kHalfBytes;
-  static constexpr int kAlpha = kP + kRowsWg * kHalfTokens * 2;
-  static constexpr int kEll = kAlpha + kRowsWg * 4;
-  static constexpr int kFlags = kEll + kRowsWg * 4;
-  static constexpr int kWaveCnt = kFlags + 4 * NW;
-  static constexpr int kList = kWaveCnt + 4 * NW;
-  static constexpr int kTotal = kList + kMaxSlotsPerSplit * 4;
+  static constexpr int kList = 2 * kBufBytes;
+  static constexpr int kWaveCnt = kList + kMaxSlotsPerSplit * 4;
+  static constexpr int kTotal = kWaveCnt + 16;
 };
-static_assert(Lds<8>::kTotal <= 160 * 1024, "LDS budget");
+static_assert(Lds::kTotal <= 160 * 1024, "LDS budget");
 
+// One direct-to-LDS load per lane: 16 bytes from src to dst + 16 * lane (dst
+// must be wave-uniform; it goes through M0).  Written as asm so that the
+// compiler does not know about the LDS writes still in flight: otherwise it
+// waits for them (vmcnt(0)) before every LDS read it cannot prove disjoint,
+// including reads of the other buffer.  The code waits for the loads
+// explicitly (vmcnt) before the barrier that publishes a buffer.
 __device__ __forceinline__ void dma16(const uint8_t* src, LDS uint8_t* dst) {
-  __builtin_amdgcn_global_load_lds((const GLOBAL void*)src, (LDS void*)dst, 16, 0, 0);
+  const uint32_t d = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(d) : "memory", "m0");
 }
 
 __device__ __forceinline__ bf16x8_t lds_b128(const LDS uint8_t* p) {
   return *(const LDS bf16x8_t*)p;
 }
 
-// Four transposing LDS reads (ds_read_b64_tr_b16) issued back to back, then
-// one wait for all of them.  Written as one asm block because the compiler
-// treats the builtin form as possibly reading the buffers that outstanding
-// direct-to-LDS prefetches write and would wait for all of them (vmcnt(0))
-// first; here those buffers are known to be disjoint from the one read.
-// The results are declared as pairs of 32-bit lanes: a 4 x 16-bit asm output
-// is not carried through whole by the compiler.
-__device__ __forceinline__ void lds_tr16_x4(i32x2_t& r0, i32x2_t& r1, i32x2_t& r2, i32x2_t& r3,
-                                            const LDS uint8_t* base, int o0, int o1, int o2,
-                                            int o3) {
-  const uint32_t b = (uint32_t)(uintptr_t)base;
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %4\n\t"
-      "ds_read_b64_tr_b16 %1, %5\n\t"
-      "ds_read_b64_tr_b16 %2, %6\n\t"
-      "ds_read_b64_tr_b16 %3, %7\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3)
-      : "v"(b + o0), "v"(b + o1), "v"(b + o2), "v"(b + o3)
-      : "memory");
-}
-
 __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// S^T products with the accumulators in architectural VGPRs.  The compiler
+// selects the accumulation-register form for every MFMA of a kernel that uses
+// accumulation registers at all, and the 256 of them hold O here; these
+// products are therefore written as inline asm with "v" operands.  MFMA
+// results are not interlocked against VALU reads: the final group pads with
+// s_nop (24 wait states, enough for a 16-pass XDL op) before the accumulators
+// are read; accumulators are only ever read by the next group's MFMAs in
+// between (7 independent MFMAs apart), and the first group starts from the
+// literal 0, so no VALU write feeds a product.
+template <int RG>
+struct SAcc {
+  f32x4_t v[RG][4];
+};
+
+template <int RG, bool kFirst, bool kLast>
+__device__ __forceinline__ void st_group(SAcc<RG>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[RG]);
+
+#define MLA_MFMA "v_mfma_f32_16x16x32_bf16 "
+template <>
+__device__ __forceinline__ void st_group<2, true, false>(SAcc<2>& c, const bf16x8_t (&a)[4],
+                                                         const bf16x8_t (&q)[2]) {
+  asm(MLA_MFMA "%0, %8, %12, 0\n\t" MLA_MFMA "%1, %9, %12, 0\n\t"
+               MLA_MFMA "%2, %10, %12, 0\n\t" MLA_MFMA "%3, %11, %12, 0\n\t"
+               MLA_MFMA "%4, %8, %13, 0\n\t" MLA_MFMA "%5, %9, %13, 0\n\t"
+               MLA_MFMA "%6, %10, %13, 0\n\t" MLA_MFMA "%7, %11, %13, 0"
+               : "=&v"(c.v[0][0]), "=&v"(c.v[0][1]), "=&v"(c.v[0][2]), "=&v"(c.v[0][3]),
+                 "=&v"(c.v[1][0]), "=&v"(c.v[1][1]), "=&v"(c.v[1][2]), "=&v"(c.v[1][3])
+               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
+}
+#define MLA_ST2                                                                        \
+  MLA_MFMA "%0, %8, %12, %0\n\t" MLA_MFMA "%1, %9, %12, %1\n\t" MLA_MFMA "%2, %10, %12, %2\n\t" \
+  MLA_MFMA "%3, %11, %12, %3\n\t" MLA_MFMA "%4, %8, %13, %4\n\t" MLA_MFMA "%5, %9, %13, %5\n\t"  \
+  MLA_MFMA "%6, %10, %13, %6\n\t" MLA_MFMA "%7, %11, %13, %7"
+template <bool kLast>
+__device__ __forceinline__ void st_group2(SAcc<2>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[2]) {
+  if (kLast)
+    asm(MLA_ST2 "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3]),
+          "+v"(c.v[1][0]), "+v"(c.v[1][1]), "+v"(c.v[1][2]), "+v"(c.v[1][3])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
+  else
+    asm(MLA_ST2
+        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3]),
+          "+v"(c.v[1][0]), "+v"(c.v[1][1]), "+v"(c.v[1][2]), "+v"(c.v[1][3])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
+}
+#undef MLA_ST2
+template <>
+__device__ __forceinline__ void st_group<2, false, false>(SAcc<2>& c, const bf16x8_t (&a)[4],
+                                                          const bf16x8_t (&q)[2]) {
+  st_group2<false>(c, a, q);
+}
+template <>
+__device__ __forceinline__ void st_group<2, false, true>(SAcc<2>& c, const bf16x8_t (&a)[4],
+                                                         const bf16x8_t (&q)[2]) {
+  st_group2<true>(c, a, q);
+}
+template <>
+__device__ __forceinline__ void st_group<1, true, false>(SAcc<1>& c, const bf16x8_t (&a)[4],
+                                                         const bf16x8_t (&q)[1]) {
+  asm(MLA_MFMA "%0, %4, %8, 0\n\t" MLA_MFMA "%1, %5, %8, 0\n\t"
+               MLA_MFMA "%2, %6, %8, 0\n\t" MLA_MFMA "%3, %7, %8, 0"
+               : "=&v"(c.v[0][0]), "=&v"(c.v[0][1]), "=&v"(c.v[0][2]), "=&v"(c.v[0][3])
+               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
+}
+#define MLA_ST1 \
+  MLA_MFMA "%0, %4, %8, %0\n\t" MLA_MFMA "%1, %5, %8, %1\n\t" MLA_MFMA "%2, %6, %8, %2\n\t" \
+  MLA_MFMA "%3, %7, %8, %3"
+template <bool kLast>
+__device__ __forceinline__ void st_group1(SAcc<1>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[1]) {
+  // With 4 accumulators a product's accumulator was written 3 MFMAs earlier;
+  // dependent same-shape accumulation chains need no extra wait states.
+  if (kLast)
+    asm(MLA_ST1 "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
+  else
+    asm(MLA_ST1
+        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
+}
+#undef MLA_ST1
+template <>
+__device__ __forceinline__ void st_group<1, false, false>(SAcc<1>& c, const bf16x8_t (&a)[4],
+                                                          const bf16x8_t (&q)[1]) {
+  st_group1<false>(c, a, q);
+}
+template <>
+__device__ __forceinline__ void st_group<1, false, true>(SAcc<1>& c, const bf16x8_t (&a)[4],
+                                                         const bf16x8_t (&q)[1]) {
+  st_group1<true>(c, a, q);
+}
+#undef MLA_MFMA
+
+// x * s for an accumulator tile that lives in the accumulation registers.
+// The empty asm statements keep the tile there: without them the register
+// allocator moves part of O into architectural VGPRs for the whole kernel to
+// serve these rare VALU uses, and spills.
+__device__ __forceinline__ f32x4_t scale_acc(f32x4_t x, float s) {
+  asm volatile("" : "+a"(x));
+  x *= s;
+  asm volatile("" : "+a"(x));
+  return x;
 }
 
 __device__ __forceinline__ float xor_max(float v) {
@@ -122,69 +203,48 @@ __device__ __forceinline__ float xor_sum(float v) {
 
 // Workgroup barrier for LDS traffic only.  __syncthreads() would also wait
 // for every outstanding vector-memory operation, including the direct-to-LDS
-// prefetches of later half-blocks; here each wave waits for its own LDS
-// reads/writes, and the prefetches are waited for explicitly by vmcnt.
+// prefetch of the next block; here each wave waits for its own LDS
+// reads/writes, and the prefetch is waited for explicitly by vmcnt.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Direct-to-LDS loads a wave issues per half-block (latent rows + RoPE rows).
-template <int NW>
-__device__ __forceinline__ int loads_per_half(int wave) {
-  return kHalfTokens / NW + (wave < 4 ? 1 : 0);
+__device__ __forceinline__ i16x4_t lds_tr16(const LDS uint8_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS i16x4_t*)p);
 }
 
-// Issue the direct-to-LDS loads of half-block `half` of pool block b:
-// wave w loads latent rows w*(32/NW) .. +32/NW-1 (1 KiB each, chunks
-// permuted by the row's swizzle) and, for w < 4, RoPE rows 8w .. 8w+7.
-template <int NW>
-__device__ __forceinline__ void issue_half(const PartialParams& p, int64_t b, int half,
-                                           LDS uint8_t* buf, int wave, int lane_in) {
-  constexpr int kRowsPerWave = kHalfTokens / NW;
+// Issue the direct-to-LDS loads of pool block b: wave w loads latent rows
+// 16w .. 16w+15 (1 KiB each, chunk c placed in slot c ^ (t & 15) = c ^ j)
+// and RoPE rows 16w .. 16w+15 (two 1 KiB loads of 8 rows).
+__device__ __forceinline__ void issue_block(const PartialParams& p, int64_t b, LDS uint8_t* buf,
+                                            int wave, int lane_in) {
   // Recompute the per-lane source offsets at every issue instead of letting
-  // them be hoisted out of the main loop: registers are the scarce resource
-  // there, and a spill would make the scratch reload wait for every
-  // outstanding prefetch.
+  // them be hoisted out of the main loop: registers are scarce there.
   int lane;
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
-  const uint8_t* ckv = p.ckv + (b * kBlock + half * kHalfTokens) * (kDLat * 2);
+  const uint8_t* ckv = p.ckv + b * kCkvBytes;
 #pragma unroll
-  for (int j = 0; j < kRowsPerWave; ++j) {
-    const int t = wave * kRowsPerWave + j;
-    const int f = (t & 15) ^ ((t & 16) >> 2);
-    dma16(ckv + t * (kDLat * 2) + ((lane ^ f) << 4), buf + t * (kDLat * 2));
+  for (int j = 0; j < 16; ++j) {
+    const int t = wave * 16 + j;
+    dma16(ckv + t * (kDLat * 2) + ((lane ^ j) << 4), buf + t * (kDLat * 2));
   }
-  if (wave < 4) {
-    const uint8_t* kpe = p.kpe + (b * kBlock + half * kHalfTokens) * (kDPe * 2);
-    const int t = wave * 8 + (lane >> 3);
+  const uint8_t* kpe = p.kpe + b * (kBlock * kDPe * 2);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
+    const int t = 8 * k + (lane >> 3);
     const int c = (lane & 7) ^ ((t >> 1) & 7);
-    dma16(kpe + t * (kDPe * 2) + (c << 4), buf + kHalfCkvBytes + wave * 1024);
+    dma16(kpe + t * (kDPe * 2) + (c << 4), buf + kCkvBytes + k * 1024);
   }
 }
 
-__device__ __forceinline__ void wait_vm(int n) {
-  // vmcnt is a 6-bit counter; n <= 2 * 9 here
-  switch (n) {
-    case 0: __builtin_amdgcn_s_waitcnt(waitcnt_vm(0)); break;
-    case 4: __builtin_amdgcn_s_waitcnt(waitcnt_vm(4)); break;
-    case 5: __builtin_amdgcn_s_waitcnt(waitcnt_vm(5)); break;
-    case 8: __builtin_amdgcn_s_waitcnt(waitcnt_vm(8)); break;
-    case 9: __builtin_amdgcn_s_waitcnt(waitcnt_vm(9)); break;
-    case 10: __builtin_amdgcn_s_waitcnt(waitcnt_vm(10)); break;
-    case 16: __builtin_amdgcn_s_waitcnt(waitcnt_vm(16)); break;
-    case 18: __builtin_amdgcn_s_waitcnt(waitcnt_vm(18)); break;
-    default: __builtin_amdgcn_s_waitcnt(waitcnt_vm(0)); break;
-  }
-}
-
-// NW waves: wave w computes S^T and the softmax for rows 16w .. 16w+15 of the
-// row tile, and O^T for latent columns w*512/NW .. (w+1)*512/NW - 1 of every
-// row of the tile.
-template <int NW>
-__global__ __launch_bounds__(NW * 64) void partial_bf16_kernel(const PartialParams p) {
-  using L = Lds<NW>;
-  constexpr int kRowsWg = L::kRowsWg;
-  constexpr int kDT = kDLat / NW / 16;  // 16-column tiles per wave
+// RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
+// of the row tile (64*RG rows) over all 512 latent columns.
+template <int RG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void partial_bf16_kernel(const PartialParams p) {
+  using L = Lds;
+  constexpr int kRowsWg = 64 * RG;
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
   LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
 
@@ -206,7 +266,7 @@ __global__ __launch_bounds__(NW * 64) void partial_bf16_kernel(const PartialPara
   LDS int* list = (LDS int*)(smem + L::kList);
   LDS int* wave_cnt = (LDS int*)(smem + L::kWaveCnt);
   int n_valid = 0;
-  for (int base = 0; base < nslots; base += NW * 64) {
+  for (int base = 0; base < nslots; base += 256) {
     const int i = base + tid;
     int b = -1;
     if (i < nslots) {
@@ -222,7 +282,7 @@ __global__ __launch_bounds__(NW * 64) void partial_bf16_kernel(const PartialPara
     __syncthreads();
     int off = n_valid, total = 0;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
+    for (int w = 0; w < 4; ++w) {
       const int c = wave_cnt[w];
       off += (w < wave) ? c : 0;
       total += c;
@@ -232,219 +292,226 @@ __global__ __launch_bounds__(NW * 64) void partial_bf16_kernel(const PartialPara
     __syncthreads();
   }
 
-  // ---- this wave's 16 query rows as MFMA B operands, held for the whole kernel
+  // ---- this wave's query rows as MFMA B operands, held for the whole kernel
   const int row_wg0 = rt * kRowsWg;
-  const int own_row_l = wave * 16 + n16;  // row within the tile owned by this lane
-  bf16x8_t qb[18];
-  {
-    const int row = row_wg0 + own_row_l;
+  bf16x8_t qb[RG][18];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
     if (row < p.rows) {
       const int i = row / p.H, h = row - (row / p.H) * p.H;
       const uint16_t* ql = p.q_lat + r * p.ql_s0 + i * p.ql_s1 + h * p.ql_s2 + g * 8;
       const uint16_t* qp = p.q_pe + r * p.qp_s0 + i * p.qp_s1 + h * p.qp_s2 + g * 8;
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks) qb[ks] = *(const bf16x8_t*)(ql + ks * 32);
+      for (int ks = 0; ks < 16; ++ks) qb[rg][ks] = *(const bf16x8_t*)(ql + ks * 32);
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) qb[16 + ks] = *(const bf16x8_t*)(qp + ks * 32);
+      for (int ks = 0; ks < 2; ++ks) qb[rg][16 + ks] = *(const bf16x8_t*)(qp + ks * 32);
     } else {
 #pragma unroll
-      for (int ks = 0; ks < 18; ++ks) qb[ks] = bf16x8_t{};
+      for (int ks = 0; ks < 18; ++ks) qb[rg][ks] = bf16x8_t{};
     }
   }
   // Q is resident before the first prefetch is issued, so that the only
-  // vector-memory operations in flight inside the main loop are prefetches.
+  // vector-memory operation in flight inside the main loop is the prefetch.
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
-  f32x4_t O[kDT][NW];
+  f32x4_t O[32][RG];
 #pragma unroll
-  for (int dt = 0; dt < kDT; ++dt)
+  for (int dt = 0; dt < 32; ++dt)
 #pragma unroll
-    for (int rg = 0; rg < NW; ++rg) O[dt][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int rg = 0; rg < RG; ++rg) O[dt][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[RG], l_run[RG];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    m_run[rg] = -INFINITY;
+    l_run[rg] = 0.f;
+  }
 
-  LDS float* alpha_lds = (LDS float*)(smem + L::kAlpha);
-  LDS int* flags = (LDS int*)(smem + L::kFlags);
-  const int my_loads = loads_per_half<NW>(wave);
-
-  // ---- main loop over half-blocks
-  const int n_half = 2 * n_valid;
-  for (int h = 0; h < n_half && h < 3; ++h)
-    issue_half<NW>(p, list[h >> 1], h & 1, smem + (h % kNumBuf) * kHalfBytes, wave, lane);
-
-  for (int h = 0; h < n_half; ++h) {
-    wait_vm(min(n_half - 1 - h, 2) * my_loads);
-    lds_barrier();  // half h is in LDS; every wave is done with half h-1
-    if (h + 3 < n_half)
-      issue_half<NW>(p, list[(h + 3) >> 1], (h + 3) & 1, smem + ((h + 3) % kNumBuf) * kHalfBytes,
-                     wave, lane);
-    const LDS uint8_t* cb = smem + (h % kNumBuf) * kHalfBytes;
+  // ---- main loop over the selected blocks: block i+1 streams in while block i
+  // is computed
+  if (n_valid > 0) issue_block(p, list[0], smem, wave, lane);
+  for (int i = 0; i < n_valid; ++i) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // block i is the only one in flight
+    lds_barrier();  // block i is in LDS for every wave; every wave is done with block i-1
+    if (i + 1 < n_valid) issue_block(p, list[i + 1], smem + ((i + 1) & 1) * kBufBytes, wave, lane);
+    const LDS uint8_t* cb = smem + (i & 1) * kBufBytes;
 
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
     // every iteration (a few VALU ops) rather than held in registers across
-    // the loop, which would push the kernel past 256 VGPRs.
+    // the loop.
     int ln = lane;
     asm volatile("" : "+v"(ln));
     const int ln16 = ln & 15, lg = ln >> 4;
 
-    // S^T[token][row] for this wave's rows, tokens 16*tau + (0..15).
-    // Key chunk 4ks+g of token 16*tau+ln16 sits in slot (4ks+g) ^ ln16 ^ 4tau,
-    // i.e. at key_base ^ ((((ks & 3) ^ tau)) << 6) + (ks >> 2) * 256.
+    // S^T[token][row], tokens 16*tau + ln16.  Latent chunk 4ks+lg of that token
+    // sits in slot (4ks+lg) ^ ln16, i.e. at key_base ^ ((ks & 3) << 6) plus
+    // (ks >> 2) * 256 within the token's row.
     const int key_base = ln16 * 1024 + ((lg ^ (ln16 & 3)) << 4) + ((ln16 >> 2) << 6);
-    const int rope_base = kHalfCkvBytes + ln16 * 128;
-    f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+    const int rope_base = kCkvBytes + ln16 * 128;
+    // 18 k-steps (2 RoPE, then 16 latent), 4 token tiles each
+    auto key_frags = [&](int step, bf16x8_t (&a)[4]) {
+      if (step < 2) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
+        for (int tau = 0; tau < 4; ++tau)
+          a[tau] = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
+      } else {
+        const int ks = step - 2;
 #pragma unroll
-      for (int tau = 0; tau < 2; ++tau)
-        acc[tau] = mfma(lds_b128(cb + tau * 2048 + rope_base + (((4 * kk + lg) ^ (ln16 >> 1)) << 4)),
-                        qb[16 + kk], acc[tau]);
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks)
-#pragma unroll
-      for (int tau = 0; tau < 2; ++tau)
-        acc[tau] = mfma(lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((((ks & 3) ^ tau)) << 6))),
-                        qb[ks], acc[tau]);
-
-    // online softmax over the half's 32 tokens, own rows (exp2 domain)
-    float tv[8];
-    float bm = -INFINITY;
-#pragma unroll
-    for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        tv[tau * 4 + i] = acc[tau][i] * p.scale_log2;
-        bm = fmaxf(bm, tv[tau * 4 + i]);
+        for (int tau = 0; tau < 4; ++tau)
+          a[tau] = lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((ks & 3) << 6)));
       }
-    bm = xor_max(bm);
-    float alpha = 1.f;
-    int rescaled = 0;
-    if (bm > m_run + kTau) {
-      if (m_run != -INFINITY) {
-        alpha = __builtin_amdgcn_exp2f(m_run - bm);
-        rescaled = 1;
-      }
-      l_run *= alpha;
-      m_run = bm;
-    }
-    if (g == 0) alpha_lds[own_row_l] = alpha;
-    float ps = 0.f;
+    };
+    auto q_of = [&](int step, bf16x8_t (&q)[RG]) {
+      const int ks = step < 2 ? 16 + step : step - 2;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      tv[k] = __builtin_amdgcn_exp2f(tv[k] - m_run);
-      ps += tv[k];
-    }
-    l_run += ps;
+      for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
+    };
+    // Software pipeline: the key fragments of step k+2 are requested before
+    // the products of step k (a ring of three fragment sets); the scheduling
+    // fences keep the compiler from regrouping loads next to their use.
+    SAcc<RG> sacc;
+    bf16x8_t ka[3][4];
+    key_frags(0, ka[0]);
+    key_frags(1, ka[1]);
 #pragma unroll
-    for (int tau = 0; tau < 2; ++tau) {
-      bf16x4_t pk;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pk[i] = (__bf16)tv[tau * 4 + i];
-      const int c = 2 * tau + (g >> 1);
-      *(LDS bf16x4_t*)(smem + L::kP + own_row_l * 64 + ((c ^ ((own_row_l >> 2) & 3)) << 4) +
-                       ((g & 1) << 3)) = pk;
+    for (int step = 0; step < 18; ++step) {
+      if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8_t q[RG];
+      q_of(step, q);
+      if (step == 0)
+        st_group<RG, true, false>(sacc, ka[0], q);
+      else if (step == 17)
+        st_group<RG, false, true>(sacc, ka[step % 3], q);
+      else
+        st_group<RG, false, false>(sacc, ka[step % 3], q);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    const int wave_rescaled = __ballot(rescaled) != 0;
-    if (lane == 0) flags[wave] = wave_rescaled;
-    lds_barrier();  // P, alpha and flags of every row are in LDS
+    f32x4_t acc[RG][4];
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+      for (int tau = 0; tau < 4; ++tau) acc[rg][tau] = sacc.v[rg][tau];
 
-    int any_flag = 0;
+    // Online softmax over the block's 64 tokens (exp2 domain).  Lane (n16, g)
+    // holds row n16 of each row group and tokens 16*tau + 4g + i.
+    bool need_any = false;
+    float bmax[RG];
 #pragma unroll
-    for (int w = 0; w < NW; ++w) any_flag |= flags[w];
-    if (any_flag) {
+    for (int rg = 0; rg < RG; ++rg) {
+      float bm = -INFINITY;
 #pragma unroll
-      for (int rg = 0; rg < NW; ++rg) {
-        const float a = alpha_lds[16 * rg + n16];
+      for (int tau = 0; tau < 4; ++tau) {
+        acc[rg][tau] *= p.scale_log2;
 #pragma unroll
-        for (int dt = 0; dt < kDT; ++dt) O[dt][rg] *= a;
+        for (int k = 0; k < 4; ++k) bm = fmaxf(bm, acc[rg][tau][k]);
       }
+      bmax[rg] = xor_max(bm);
+      need_any |= bmax[rg] > m_run[rg] + kTau;
     }
-    // Transposing value reads: lane (g, r4 = (lane>>2)&3, q4 = lane&3) supplies
-    // token 8g + 4hh + r4 and latent columns 16*ct + 4*q4 .. +3; the result
-    // gives lane n16 column 16*ct + n16 of four consecutive tokens.
-    int lv = lane;
-    asm volatile("" : "+v"(lv));
-    const int r4 = (lv >> 2) & 3, q4 = lv & 3, vg = lv >> 4;
-    int tr_off[2];
+    if (__ballot(need_any) != 0) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int t = 8 * vg + 4 * hh + r4;
-      const int f = (t & 15) ^ ((t & 16) >> 2);
-      const int c0 = 2 * wave * kDT + (q4 >> 1);  // chunk of column tile ct = wave*kDT
-      // chunk 2*dt + c0 of token t sits in slot (c0 + 2dt) ^ f; the 2dt bits
-      // are disjoint from c0's, so the slot is ((c0 ^ f) ^ 2dt) within the
-      // 16-chunk group of c0
-      tr_off[hh] = t * 1024 + ((q4 & 1) << 3) + (((c0 & ~15) | ((c0 & 15) ^ f)) << 4);
-    }
-    bf16x8_t va[kDT];
+      for (int rg = 0; rg < RG; ++rg) {
+        float alpha = 1.f;
+        if (bmax[rg] > m_run[rg] + kTau) {
+          if (m_run[rg] != -INFINITY) alpha = __builtin_amdgcn_exp2f(m_run[rg] - bmax[rg]);
+          m_run[rg] = bmax[rg];
+          l_run[rg] *= alpha;
+        }
+        if (__ballot(alpha != 1.f) != 0) {
 #pragma unroll
-    for (int dt = 0; dt < kDT; dt += 2) {
-      i32x2_t lo0, hi0, lo1, hi1;
-      lds_tr16_x4(lo0, hi0, lo1, hi1, cb, tr_off[0] ^ (dt << 5), tr_off[1] ^ (dt << 5),
-                  tr_off[0] ^ ((dt + 1) << 5), tr_off[1] ^ ((dt + 1) << 5));
-      va[dt] = __builtin_bit_cast(bf16x8_t, i32x4_t{lo0[0], lo0[1], hi0[0], hi0[1]});
-      va[dt + 1] = __builtin_bit_cast(bf16x8_t, i32x4_t{lo1[0], lo1[1], hi1[0], hi1[1]});
-    }
-    // P tile (rows x 32 tokens, bf16, 64 B per row): row 16*rg + n16 of the
-    // tile at p_rd + rg * 1024 (its swizzle only depends on n16)
-    const int p_rd = L::kP + (lv & 15) * 64 + ((vg ^ (((lv & 15) >> 2) & 3)) << 4);
-#pragma unroll
-    for (int rg = 0; rg < NW; ++rg) {
-      const bf16x8_t pb = lds_b128(smem + p_rd + rg * 1024);
-#pragma unroll
-      for (int dt = 0; dt < kDT; ++dt) O[dt][rg] = mfma(va[dt], pb, O[dt][rg]);
-    }
-  }
-
-  // ---- epilogue: row statistics of own rows, then every wave normalises its columns
-  LDS float* ell_lds = (LDS float*)(smem + L::kEll);
-  const bool direct = p.n_splits == 1;
-  const int64_t part = (int64_t)r * p.n_splits + s_idx;
-  {
-    const float l_tot = xor_sum(l_run);
-    const int row = row_wg0 + own_row_l;
-    if (g == 0) {
-      ell_lds[own_row_l] = l_tot;
-      if (row < p.rows) {
-        const float lse = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
-        if (direct) {
-          const int i = row / p.H, hd = row - (row / p.H) * p.H;
-          p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
-        } else {
-          p.ws_lse[part * p.rows + row] = lse;
+          for (int dt = 0; dt < 32; ++dt) O[dt][rg] = scale_acc(O[dt][rg], alpha);
         }
       }
     }
-  }
-  __syncthreads();
+    // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}
+    bf16x8_t pb[RG][2];
 #pragma unroll
-  for (int rg = 0; rg < NW; ++rg) {
-    const int row = row_wg0 + 16 * rg + n16;
+    for (int rg = 0; rg < RG; ++rg) {
+      float ps = 0.f;
+#pragma unroll
+      for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float e = __builtin_amdgcn_exp2f(acc[rg][tau][k] - m_run[rg]);
+          ps += e;
+          pb[rg][tau >> 1][(tau & 1) * 4 + k] = (__bf16)e;
+        }
+      l_run[rg] += ps;
+    }
+
+    // O^T[dim][row] += V^T . P^T.  Value rows for lane (g, r4, q4): token
+    // 32ps + 16hh + 4g + r4 (= 32ps + 16hh + (lane >> 2)), latent columns
+    // 16dt + 4q4 .. +3, i.e. chunk 2dt + (q4 >> 1) of a row whose swizzle key is
+    // x = lane >> 2.  The slot (2dt + (q4>>1)) ^ x splits into a per-lane part
+    // and (dt & 7) << 1 XORed into bits 1..3, plus the 16-chunk group dt >> 3.
+    int lv = lane;
+    asm volatile("" : "+v"(lv));
+    const int x = lv >> 2, q4 = lv & 3;
+    const int tr_base = x * 1024 + ((2 * (x >> 1) + ((q4 >> 1) ^ (x & 1))) << 4) + ((q4 & 1) << 3);
+    auto tr_off = [&](int ps, int hh, int dt) {
+      return (tr_base ^ ((dt & 7) << 5)) + (dt >> 3) * 256 + ps * 32768 + hh * 16384;
+    };
+    // 64 value fragments (2 k-steps x 32 column tiles) in a software pipeline
+    // kPvAhead fragments deep.
+    constexpr int kPvAhead = 8;
+    auto v_frag = [&](int f) {
+      const int ps = f >> 5, dt = f & 31;
+      const i16x4_t lo = lds_tr16(cb + tr_off(ps, 0, dt));
+      const i16x4_t hi = lds_tr16(cb + tr_off(ps, 1, dt));
+      return __builtin_bit_cast(bf16x8_t,
+                                i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+    };
+    bf16x8_t va[kPvAhead + 1];
+#pragma unroll
+    for (int f = 0; f < kPvAhead; ++f) va[f] = v_frag(f);
+#pragma unroll
+    for (int f = 0; f < 64; ++f) {
+      if (f + kPvAhead < 64) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
+      __builtin_amdgcn_sched_barrier(0);
+      const int ps = f >> 5, dt = f & 31;
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg)
+        O[dt][rg] = mfma(va[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // ---- epilogue
+  const bool direct = p.n_splits == 1;
+  const int64_t part = (int64_t)r * p.n_splits + s_idx;
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const float l_tot = xor_sum(l_run[rg]);
+    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
     if (row >= p.rows) continue;
-    const float l_tot = ell_lds[16 * rg + n16];
+    const float lse = l_tot > 0.f ? (m_run[rg] + __log2f(l_tot)) * kLn2 : -INFINITY;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     float* dst;
     if (direct) {
       const int i = row / p.H, hd = row - (row / p.H) * p.H;
       dst = p.out + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
+      if (g == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
     } else {
       dst = p.ws_o + (part * p.rows + row) * kDLat;
+      if (g == 0) p.ws_lse[part * p.rows + row] = lse;
     }
-    dst += wave * (kDT * 16) + 4 * g;
+    dst += 4 * g;
 #pragma unroll
-    for (int dt = 0; dt < kDT; ++dt) *(f32x4_t*)(dst + dt * 16) = O[dt][rg] * inv;
+    for (int dt = 0; dt < 32; ++dt) *(f32x4_t*)(dst + dt * 16) = scale_acc(O[dt][rg], inv);
   }
 }
 
 }  // namespace
 
-hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int waves, hipStream_t s) {
+hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s) {
   if (fp8) return hipErrorNotSupported;
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (waves == 8)
-    hipLaunchKernelGGL(partial_bf16_kernel<8>, dim3(grid), dim3(8 * 64), 0, s, p);
+  if (row_groups == 2)
+    hipLaunchKernelGGL(partial_bf16_kernel<2>, dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(partial_bf16_kernel<4>, dim3(grid), dim3(4 * 64), 0, s, p);
+    hipLaunchKernelGGL(partial_bf16_kernel<1>, dim3(grid), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
