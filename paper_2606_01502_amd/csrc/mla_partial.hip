@@ -50,9 +50,19 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
 
-constexpr int kCkvBytes = kBlock * kDLat * 2;           // 64 KiB of latent rows
-constexpr int kBufBytes = kCkvBytes + kBlock * kDPe * 2;  // + 8 KiB of RoPE rows
-constexpr int kLoadsPerBlock = 18;  // per wave: 16 latent rows + 2 KiB of RoPE rows
+// Blocks stream through a ring of LDS stages of TOK tokens (TOK = 32: four
+// stages, up to three in flight; TOK = 64: two stages).  A stage holds TOK
+// latent rows (1 KiB each) followed by TOK RoPE rows (128 B each).
+constexpr int kRingBytes = 2 * kBlock * (kDLat + kDPe) * 2;  // 144 KiB
+template <int TOK>
+struct Stage {
+  static constexpr int kNum = kRingBytes / (TOK * (kDLat + kDPe) * 2);
+  static constexpr int kCkv = TOK * kDLat * 2;
+  static constexpr int kBytes = kCkv + TOK * kDPe * 2;
+  static constexpr int kPerBlock = kBlock / TOK;
+  // direct-to-LDS loads per wave per stage: TOK/4 latent rows + TOK/32 KiB of RoPE rows
+  static constexpr int kLoads = TOK / 4 + TOK / 32;
+};
 constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -60,7 +70,7 @@ constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 struct Lds {
-  static constexpr int kList = 2 * kBufBytes;
+  static constexpr int kList = kRingBytes;
   static constexpr int kWaveCnt = kList + kMaxSlotsPerSplit * 4;
   static constexpr int kTotal = kWaveCnt + 16;
 };
@@ -95,89 +105,83 @@ __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 // are read; accumulators are only ever read by the next group's MFMAs in
 // between (7 independent MFMAs apart), and the first group starts from the
 // literal 0, so no VALU write feeds a product.
-template <int RG>
-struct SAcc {
-  f32x4_t v[RG][4];
-};
-
-template <int RG, bool kFirst, bool kLast>
-__device__ __forceinline__ void st_group(SAcc<RG>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[RG]);
-
 #define MLA_MFMA "v_mfma_f32_16x16x32_bf16 "
-template <>
-__device__ __forceinline__ void st_group<2, true, false>(SAcc<2>& c, const bf16x8_t (&a)[4],
-                                                         const bf16x8_t (&q)[2]) {
-  asm(MLA_MFMA "%0, %8, %12, 0\n\t" MLA_MFMA "%1, %9, %12, 0\n\t"
-               MLA_MFMA "%2, %10, %12, 0\n\t" MLA_MFMA "%3, %11, %12, 0\n\t"
-               MLA_MFMA "%4, %8, %13, 0\n\t" MLA_MFMA "%5, %9, %13, 0\n\t"
-               MLA_MFMA "%6, %10, %13, 0\n\t" MLA_MFMA "%7, %11, %13, 0"
-               : "=&v"(c.v[0][0]), "=&v"(c.v[0][1]), "=&v"(c.v[0][2]), "=&v"(c.v[0][3]),
-                 "=&v"(c.v[1][0]), "=&v"(c.v[1][1]), "=&v"(c.v[1][2]), "=&v"(c.v[1][3])
-               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
-}
-#define MLA_ST2                                                                        \
-  MLA_MFMA "%0, %8, %12, %0\n\t" MLA_MFMA "%1, %9, %12, %1\n\t" MLA_MFMA "%2, %10, %12, %2\n\t" \
-  MLA_MFMA "%3, %11, %12, %3\n\t" MLA_MFMA "%4, %8, %13, %4\n\t" MLA_MFMA "%5, %9, %13, %5\n\t"  \
-  MLA_MFMA "%6, %10, %13, %6\n\t" MLA_MFMA "%7, %11, %13, %7"
-template <bool kLast>
-__device__ __forceinline__ void st_group2(SAcc<2>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[2]) {
-  if (kLast)
-    asm(MLA_ST2 "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
-        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3]),
-          "+v"(c.v[1][0]), "+v"(c.v[1][1]), "+v"(c.v[1][2]), "+v"(c.v[1][3])
-        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
-  else
-    asm(MLA_ST2
-        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3]),
-          "+v"(c.v[1][0]), "+v"(c.v[1][1]), "+v"(c.v[1][2]), "+v"(c.v[1][3])
-        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]));
-}
-#undef MLA_ST2
-template <>
-__device__ __forceinline__ void st_group<2, false, false>(SAcc<2>& c, const bf16x8_t (&a)[4],
-                                                          const bf16x8_t (&q)[2]) {
-  st_group2<false>(c, a, q);
-}
-template <>
-__device__ __forceinline__ void st_group<2, false, true>(SAcc<2>& c, const bf16x8_t (&a)[4],
-                                                         const bf16x8_t (&q)[2]) {
-  st_group2<true>(c, a, q);
-}
-template <>
-__device__ __forceinline__ void st_group<1, true, false>(SAcc<1>& c, const bf16x8_t (&a)[4],
-                                                         const bf16x8_t (&q)[1]) {
-  asm(MLA_MFMA "%0, %4, %8, 0\n\t" MLA_MFMA "%1, %5, %8, 0\n\t"
-               MLA_MFMA "%2, %6, %8, 0\n\t" MLA_MFMA "%3, %7, %8, 0"
-               : "=&v"(c.v[0][0]), "=&v"(c.v[0][1]), "=&v"(c.v[0][2]), "=&v"(c.v[0][3])
-               : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
-}
-#define MLA_ST1 \
-  MLA_MFMA "%0, %4, %8, %0\n\t" MLA_MFMA "%1, %5, %8, %1\n\t" MLA_MFMA "%2, %6, %8, %2\n\t" \
-  MLA_MFMA "%3, %7, %8, %3"
-template <bool kLast>
-__device__ __forceinline__ void st_group1(SAcc<1>& c, const bf16x8_t (&a)[4], const bf16x8_t (&q)[1]) {
-  // With 4 accumulators a product's accumulator was written 3 MFMAs earlier;
-  // dependent same-shape accumulation chains need no extra wait states.
-  if (kLast)
-    asm(MLA_ST1 "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
-        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3])
-        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
-  else
-    asm(MLA_ST1
-        : "+v"(c.v[0][0]), "+v"(c.v[0][1]), "+v"(c.v[0][2]), "+v"(c.v[0][3])
-        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]));
-}
-#undef MLA_ST1
-template <>
-__device__ __forceinline__ void st_group<1, false, false>(SAcc<1>& c, const bf16x8_t (&a)[4],
-                                                          const bf16x8_t (&q)[1]) {
-  st_group1<false>(c, a, q);
-}
-template <>
-__device__ __forceinline__ void st_group<1, false, true>(SAcc<1>& c, const bf16x8_t (&a)[4],
-                                                         const bf16x8_t (&q)[1]) {
-  st_group1<true>(c, a, q);
-}
+
+// One k-step of S^T for RG row groups x NT token tiles, as one asm statement:
+// c[rg][tau] += a[tau] . q[rg].  kFirst starts from the literal 0; kLast pads
+// with 24 wait states so the results may be read by VALU code (MFMA results
+// are not interlocked against VALU reads).  Accumulators of consecutive
+// groups are RG*NT - 1 >= 3 independent products apart.
+template <int RG, int NT, bool kFirst, bool kLast>
+struct StGroup;
+
+#define MLA_NOPS "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+// RG = 2, NT = 4: %0..%7 accumulators (rg-major), %8..%11 keys, %12..%13 queries
+#define MLA_G24(C) \
+  MLA_MFMA "%0, %8, %12, " C(0) "\n\t" MLA_MFMA "%1, %9, %12, " C(1) "\n\t"    \
+  MLA_MFMA "%2, %10, %12, " C(2) "\n\t" MLA_MFMA "%3, %11, %12, " C(3) "\n\t"  \
+  MLA_MFMA "%4, %8, %13, " C(4) "\n\t" MLA_MFMA "%5, %9, %13, " C(5) "\n\t"    \
+  MLA_MFMA "%6, %10, %13, " C(6) "\n\t" MLA_MFMA "%7, %11, %13, " C(7)
+// RG = 2, NT = 2: %0..%3 accumulators, %4..%5 keys, %6..%7 queries
+#define MLA_G22(C) \
+  MLA_MFMA "%0, %4, %6, " C(0) "\n\t" MLA_MFMA "%1, %5, %6, " C(1) "\n\t" \
+  MLA_MFMA "%2, %4, %7, " C(2) "\n\t" MLA_MFMA "%3, %5, %7, " C(3)
+// RG = 1, NT = 4: %0..%3 accumulators, %4..%7 keys, %8 query
+#define MLA_G14(C) \
+  MLA_MFMA "%0, %4, %8, " C(0) "\n\t" MLA_MFMA "%1, %5, %8, " C(1) "\n\t" \
+  MLA_MFMA "%2, %6, %8, " C(2) "\n\t" MLA_MFMA "%3, %7, %8, " C(3)
+#define MLA_ZERO(i) "0"
+#define MLA_ACC0 "%0"
+#define MLA_ACC1 "%1"
+#define MLA_ACC2 "%2"
+#define MLA_ACC3 "%3"
+#define MLA_ACC4 "%4"
+#define MLA_ACC5 "%5"
+#define MLA_ACC6 "%6"
+#define MLA_ACC7 "%7"
+#define MLA_ACC(i) MLA_ACC##i
+#define MLA_OUT24(m) m(c[0][0]), m(c[0][1]), m(c[0][2]), m(c[0][3]), \
+                     m(c[1][0]), m(c[1][1]), m(c[1][2]), m(c[1][3])
+#define MLA_OUT22(m) m(c[0][0]), m(c[0][1]), m(c[1][0]), m(c[1][1])
+#define MLA_OUT14(m) m(c[0][0]), m(c[0][1]), m(c[0][2]), m(c[0][3])
+#define MLA_W(x) "=&v"(x)
+#define MLA_RW(x) "+v"(x)
+#define MLA_STGROUP(RG_, NT_, G, OUTS, ...)                                                 \
+  template <bool kLast>                                                                     \
+  struct StGroup<RG_, NT_, true, kLast> {                                                   \
+    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
+                                               const bf16x8_t (&a)[NT_],                    \
+                                               const bf16x8_t (&q)[RG_]) {                  \
+      asm(G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                                         \
+    }                                                                                       \
+  };                                                                                        \
+  template <>                                                                               \
+  struct StGroup<RG_, NT_, false, false> {                                                  \
+    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
+                                               const bf16x8_t (&a)[NT_],                    \
+                                               const bf16x8_t (&q)[RG_]) {                  \
+      asm(G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                                         \
+    }                                                                                       \
+  };                                                                                        \
+  template <>                                                                               \
+  struct StGroup<RG_, NT_, false, true> {                                                   \
+    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
+                                               const bf16x8_t (&a)[NT_],                    \
+                                               const bf16x8_t (&q)[RG_]) {                  \
+      asm(G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                                \
+    }                                                                                       \
+  };
+MLA_STGROUP(2, 4, MLA_G24, MLA_OUT24, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]))
+MLA_STGROUP(2, 2, MLA_G22, MLA_OUT22, "v"(a[0]), "v"(a[1]), "v"(q[0]), "v"(q[1]))
+MLA_STGROUP(1, 4, MLA_G14, MLA_OUT14, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]))
+#undef MLA_STGROUP
+#undef MLA_G24
+#undef MLA_G22
+#undef MLA_G14
+#undef MLA_OUT24
+#undef MLA_OUT22
+#undef MLA_OUT14
+#undef MLA_NOPS
 #undef MLA_MFMA
 
 // x * s for an accumulator tile that lives in the accumulation registers.
@@ -213,36 +217,54 @@ __device__ __forceinline__ i16x4_t lds_tr16(const LDS uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS i16x4_t*)p);
 }
 
-// Issue the direct-to-LDS loads of pool block b: wave w loads latent rows
-// 16w .. 16w+15 (1 KiB each, chunk c placed in slot c ^ (t & 15) = c ^ j)
-// and RoPE rows 16w .. 16w+15 (two 1 KiB loads of 8 rows).
-__device__ __forceinline__ void issue_block(const PartialParams& p, int64_t b, LDS uint8_t* buf,
-                                            int wave, int lane_in) {
+// Issue the direct-to-LDS loads of tokens part*TOK .. part*TOK+TOK-1 of pool
+// block b into a stage: wave w loads latent rows w*TOK/4 .. (w+1)*TOK/4-1 of
+// the stage (1 KiB each, chunk c placed in slot c ^ (t & 15)) and 1 KiB
+// groups of 8 RoPE rows w*TOK/32 .. (w+1)*TOK/32-1.
+template <int TOK>
+__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, int part,
+                                            LDS uint8_t* buf, int wave, int lane_in) {
   // Recompute the per-lane source offsets at every issue instead of letting
   // them be hoisted out of the main loop: registers are scarce there.
   int lane;
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
-  const uint8_t* ckv = p.ckv + b * kCkvBytes;
+  const int64_t tok0 = b * kBlock + part * TOK;
+  const uint8_t* ckv = p.ckv + tok0 * (kDLat * 2);
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const int t = wave * 16 + j;
-    dma16(ckv + t * (kDLat * 2) + ((lane ^ j) << 4), buf + t * (kDLat * 2));
+  for (int j = 0; j < TOK / 4; ++j) {
+    const int t = wave * (TOK / 4) + j;
+    dma16(ckv + t * (kDLat * 2) + ((lane ^ (t & 15)) << 4), buf + t * (kDLat * 2));
   }
-  const uint8_t* kpe = p.kpe + b * (kBlock * kDPe * 2);
+  const uint8_t* kpe = p.kpe + tok0 * (kDPe * 2);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
+  for (int j = 0; j < TOK / 32; ++j) {
+    const int k = wave * (TOK / 32) + j;  // 1 KiB = RoPE rows 8k .. 8k+7
     const int t = 8 * k + (lane >> 3);
     const int c = (lane & 7) ^ ((t >> 1) & 7);
-    dma16(kpe + t * (kDPe * 2) + (c << 4), buf + kCkvBytes + k * 1024);
+    dma16(kpe + t * (kDPe * 2) + (c << 4), buf + Stage<TOK>::kCkv + k * 1024);
   }
+}
+
+// Wait until at most `stages` later stages of this wave's loads are in flight.
+template <int TOK>
+__device__ __forceinline__ void wait_stages(int stages) {
+  constexpr int L = Stage<TOK>::kLoads;
+  if (stages >= 2)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * L));
+  else if (stages == 1)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(L));
+  else
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 }
 
 // RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
 // of the row tile (64*RG rows) over all 512 latent columns.
-template <int RG>
+template <int RG, int TOK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void partial_bf16_kernel(const PartialParams p) {
+  using St = Stage<TOK>;
+  constexpr int kTau4 = TOK / 16;  // 16-token tiles per stage
+  constexpr int kKSteps = TOK / 32;  // 32-token PV k-steps per stage
   using L = Lds;
   constexpr int kRowsWg = 64 * RG;
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
@@ -327,14 +349,26 @@ void partial_bf16_kernel(const PartialParams p) {
     l_run[rg] = 0.f;
   }
 
-  // ---- main loop over the selected blocks: block i+1 streams in while block i
+  // ---- main loop over stages: up to St::kNum - 1 stages stream in while one
   // is computed
-  if (n_valid > 0) issue_block(p, list[0], smem, wave, lane);
-  for (int i = 0; i < n_valid; ++i) {
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // block i is the only one in flight
-    lds_barrier();  // block i is in LDS for every wave; every wave is done with block i-1
-    if (i + 1 < n_valid) issue_block(p, list[i + 1], smem + ((i + 1) & 1) * kBufBytes, wave, lane);
-    const LDS uint8_t* cb = smem + (i & 1) * kBufBytes;
+  const int n_stage = n_valid * St::kPerBlock;
+  for (int h = 0; h < n_stage && h < St::kNum - 1; ++h)
+    issue_stage<TOK>(p, list[h / St::kPerBlock], h % St::kPerBlock, smem + h * St::kBytes, wave,
+                     lane);
+  for (int h = 0; h < n_stage; ++h) {
+    wait_stages<TOK>(min(n_stage - 1 - h, St::kNum - 2));
+    lds_barrier();  // stage h is in LDS for every wave; every wave is done with stage h-1
+    {
+      // All of the next stage's loads at once: spreading them between the
+      // products measured slower (each load holds the issuing wave until the
+      // shared address unit takes it, and the stage's LDS reads then compete
+      // with the incoming writes).
+      const int hn = h + St::kNum - 1;
+      if (hn < n_stage)
+        issue_stage<TOK>(p, list[hn / St::kPerBlock], hn % St::kPerBlock,
+                         smem + (hn % St::kNum) * St::kBytes, wave, lane);
+    }
+    const LDS uint8_t* cb = smem + (h % St::kNum) * St::kBytes;
 
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
     // every iteration (a few VALU ops) rather than held in registers across
@@ -347,53 +381,50 @@ void partial_bf16_kernel(const PartialParams p) {
     // sits in slot (4ks+lg) ^ ln16, i.e. at key_base ^ ((ks & 3) << 6) plus
     // (ks >> 2) * 256 within the token's row.
     const int key_base = ln16 * 1024 + ((lg ^ (ln16 & 3)) << 4) + ((ln16 >> 2) << 6);
-    const int rope_base = kCkvBytes + ln16 * 128;
+    const int rope_base = St::kCkv + ln16 * 128;
     // 18 k-steps (2 RoPE, then 16 latent), 4 token tiles each
-    auto key_frags = [&](int step, bf16x8_t (&a)[4]) {
+    auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
       if (step < 2) {
 #pragma unroll
-        for (int tau = 0; tau < 4; ++tau)
+        for (int tau = 0; tau < kTau4; ++tau)
           a[tau] = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
       } else {
         const int ks = step - 2;
 #pragma unroll
-        for (int tau = 0; tau < 4; ++tau)
+        for (int tau = 0; tau < kTau4; ++tau)
           a[tau] = lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((ks & 3) << 6)));
       }
-    };
-    auto q_of = [&](int step, bf16x8_t (&q)[RG]) {
-      const int ks = step < 2 ? 16 + step : step - 2;
-#pragma unroll
-      for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
     };
     // Software pipeline: the key fragments of step k+2 are requested before
     // the products of step k (a ring of three fragment sets); the scheduling
     // fences keep the compiler from regrouping loads next to their use.
-    SAcc<RG> sacc;
-    bf16x8_t ka[3][4];
+    f32x4_t sacc[RG][kTau4];
+    bf16x8_t ka[3][kTau4];
     key_frags(0, ka[0]);
     key_frags(1, ka[1]);
 #pragma unroll
     for (int step = 0; step < 18; ++step) {
       if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
       __builtin_amdgcn_sched_barrier(0);
+      const int ks = step < 2 ? 16 + step : step - 2;
       bf16x8_t q[RG];
-      q_of(step, q);
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
       if (step == 0)
-        st_group<RG, true, false>(sacc, ka[0], q);
+        StGroup<RG, kTau4, true, false>::run(sacc, ka[0], q);
       else if (step == 17)
-        st_group<RG, false, true>(sacc, ka[step % 3], q);
+        StGroup<RG, kTau4, false, true>::run(sacc, ka[step % 3], q);
       else
-        st_group<RG, false, false>(sacc, ka[step % 3], q);
+        StGroup<RG, kTau4, false, false>::run(sacc, ka[step % 3], q);
       __builtin_amdgcn_sched_barrier(0);
     }
-    f32x4_t acc[RG][4];
+    f32x4_t acc[RG][kTau4];
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
-      for (int tau = 0; tau < 4; ++tau) acc[rg][tau] = sacc.v[rg][tau];
+      for (int tau = 0; tau < kTau4; ++tau) acc[rg][tau] = sacc[rg][tau];
 
-    // Online softmax over the block's 64 tokens (exp2 domain).  Lane (n16, g)
+    // Online softmax over the stage's TOK tokens (exp2 domain).  Lane (n16, g)
     // holds row n16 of each row group and tokens 16*tau + 4g + i.
     bool need_any = false;
     float bmax[RG];
@@ -401,7 +432,7 @@ void partial_bf16_kernel(const PartialParams p) {
     for (int rg = 0; rg < RG; ++rg) {
       float bm = -INFINITY;
 #pragma unroll
-      for (int tau = 0; tau < 4; ++tau) {
+      for (int tau = 0; tau < kTau4; ++tau) {
         acc[rg][tau] *= p.scale_log2;
 #pragma unroll
         for (int k = 0; k < 4; ++k) bm = fmaxf(bm, acc[rg][tau][k]);
@@ -425,12 +456,12 @@ void partial_bf16_kernel(const PartialParams p) {
       }
     }
     // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}
-    bf16x8_t pb[RG][2];
+    bf16x8_t pb[RG][kKSteps];
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
       float ps = 0.f;
 #pragma unroll
-      for (int tau = 0; tau < 4; ++tau)
+      for (int tau = 0; tau < kTau4; ++tau)
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const float e = __builtin_amdgcn_exp2f(acc[rg][tau][k] - m_run[rg]);
@@ -452,9 +483,10 @@ void partial_bf16_kernel(const PartialParams p) {
     auto tr_off = [&](int ps, int hh, int dt) {
       return (tr_base ^ ((dt & 7) << 5)) + (dt >> 3) * 256 + ps * 32768 + hh * 16384;
     };
-    // 64 value fragments (2 k-steps x 32 column tiles) in a software pipeline
-    // kPvAhead fragments deep.
+    // kKSteps x 32 value fragments (k-steps x column tiles) in a software
+    // pipeline kPvAhead fragments deep.
     constexpr int kPvAhead = 8;
+    constexpr int kFrags = 32 * kKSteps;
     auto v_frag = [&](int f) {
       const int ps = f >> 5, dt = f & 31;
       const i16x4_t lo = lds_tr16(cb + tr_off(ps, 0, dt));
@@ -466,8 +498,8 @@ void partial_bf16_kernel(const PartialParams p) {
 #pragma unroll
     for (int f = 0; f < kPvAhead; ++f) va[f] = v_frag(f);
 #pragma unroll
-    for (int f = 0; f < 64; ++f) {
-      if (f + kPvAhead < 64) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
+    for (int f = 0; f < kFrags; ++f) {
+      if (f + kPvAhead < kFrags) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
       __builtin_amdgcn_sched_barrier(0);
       const int ps = f >> 5, dt = f & 31;
 #pragma unroll
@@ -504,14 +536,18 @@ void partial_bf16_kernel(const PartialParams p) {
 
 }  // namespace
 
+#ifndef MLA_STAGE_TOKENS
+#define MLA_STAGE_TOKENS 64
+#endif
+
 hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s) {
   if (fp8) return hipErrorNotSupported;
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
   if (row_groups == 2)
-    hipLaunchKernelGGL(partial_bf16_kernel<2>, dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_bf16_kernel<2, MLA_STAGE_TOKENS>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(partial_bf16_kernel<1>, dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_bf16_kernel<1, 64>), dim3(grid), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
