@@ -6,11 +6,12 @@
  * Method: "Move the Query, Not the Cache" (arXiv 2606.01502).  A requester
  * ships absorbed-MLA query rows, each d_qk = 576 wide (a 512-wide latent part
  * and a 64-wide decoupled-RoPE part), to the instance holding a cached chunk;
- * the holder attends them over the chunk's resident latent cache and returns a
- * d_v = 512 wide partial output with the statistics that let the requester
- * merge it exactly (Section 3.2, wire format).  Under sparse selection the
- * holder attends only the entries the indexer selected, at their canonical
- * positions (Sections 3.3, 5.4, 6.3).  The requester recombines partials by
+ * the holder attends them over the chunk's latent cache that it keeps in
+ * memory and returns a d_v = 512 wide partial output together with softmax
+ * statistics from which the requester can recombine partials exactly
+ * (Section 3.2, wire format).  Under sparse selection the holder attends only
+ * the entries the indexer picked, each at the position it was cached at
+ * (Sections 3.3, 5.4, 6.3).  The requester recombines partials by
  * online softmax; the merge is commutative and has a zero-weight identity
  * (Sections 2.2 and 3.3).
  *

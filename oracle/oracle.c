@@ -12,13 +12,14 @@
  *     wide (a 512-wide latent part and a 64-wide decoupled-RoPE part) and
  *     the partial output row is d_v = 512 wide.  Reading: key = [ckv ; kpe]
  *     (576), value = ckv (512); the up/down projections are absorbed outside.
- *   - Section 3.2: the holder returns its attention over the resident
- *     subset plus the running max logit and softmax denominator, which let
- *     the requester merge it exactly.  Here that statistic is returned as the
- *     normalised output row and lse = max + ln(denominator) (natural log).
- *   - Section 3.2: the holder is position-oblivious (the requester rotates
- *     the query), and Section 3.3: selected entries are attended at their
- *     canonical positions.  So there is no mask and no rotation here.
+ *   - Section 3.2: the holder sends back the softmax-weighted latent row for
+ *     the keys it holds together with the two softmax statistics (maximum
+ *     logit, denominator) that make an exact recombination possible.  Here
+ *     those statistics are folded into lse = max + ln(denominator), natural
+ *     log, next to the normalised output row.
+ *   - Section 3.2: any positional rotation of the query happens at the
+ *     requester, and Section 3.3: a selected cache entry keeps the position
+ *     it was cached at.  So the holder applies no mask and no rotation.
  *   - Section 3.3 and Section 6.3: the selection-regime holder attends only
  *     the indexer's selected entries; here selection is by 64-token blocks.
  *   - Section 2.2 and Section 3.3: partials are recombined by online softmax;
