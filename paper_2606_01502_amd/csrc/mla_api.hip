@@ -203,9 +203,13 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the int32 index range");
 
     const Extent outs[2] = {extent(*out_lat), extent(*out_lse)};
-    const Extent ins[7] = {extent(*q_lat), extent(*q_pe), extent(*ckv_pool), extent(*kpe_pool),
+    auto scale_extent = [&](const float* sc) -> Extent {
+      if (!fp8 || P == 0) return {0, 0};
+      return {(uintptr_t)sc, (uintptr_t)(sc + P)};
+    };
+    const Extent ins[8] = {extent(*q_lat), extent(*q_pe), extent(*ckv_pool), extent(*kpe_pool),
                            extent(*chunk_block_table), extent(*sel_block_ids),
-                           {0, 0}};
+                           scale_extent(ckv_pool->block_scale), scale_extent(kpe_pool->block_scale)};
     if (overlaps(outs[0], outs[1])) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat and out_lse overlap");
     for (const Extent& o : outs)
       for (const Extent& i : ins)
@@ -213,7 +217,6 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
 
     const int64_t rows = Mq * H;
     if (R == 0 || rows == 0) return MLA_OK;
-    if (fp8) return fail(MLA_ERR_UNSUPPORTED, "fp8-e4m3fn pools are not implemented in this build");
 
     // ---- plan: row tiles of 128 or 64 rows (4 waves of 32 or 16 rows);
     // split-K over slot ranges so that the grid covers the chip

@@ -46,22 +46,26 @@ typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef short i16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
 
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
 
-// Blocks stream through a ring of LDS stages of TOK tokens (TOK = 32: four
-// stages, up to three in flight; TOK = 64: two stages).  A stage holds TOK
-// latent rows (1 KiB each) followed by TOK RoPE rows (128 B each).
+// Blocks stream through a ring of LDS stages of one 64-token block each: the
+// block's latent rows followed by its RoPE rows.  bf16: 73,728 B per stage,
+// two stages.  fp8 (e4m3 codes): 36,864 B per stage, four stages.
 constexpr int kRingBytes = 2 * kBlock * (kDLat + kDPe) * 2;  // 144 KiB
-template <int TOK>
+template <bool FP8>
 struct Stage {
-  static constexpr int kNum = kRingBytes / (TOK * (kDLat + kDPe) * 2);
-  static constexpr int kCkv = TOK * kDLat * 2;
-  static constexpr int kBytes = kCkv + TOK * kDPe * 2;
-  static constexpr int kPerBlock = kBlock / TOK;
-  // direct-to-LDS loads per wave per stage: TOK/4 latent rows + TOK/32 KiB of RoPE rows
-  static constexpr int kLoads = TOK / 4 + TOK / 32;
+  static constexpr int kElt = FP8 ? 1 : 2;
+  static constexpr int kRowCkv = kDLat * kElt;  // bytes per latent row
+  static constexpr int kRowKpe = kDPe * kElt;
+  static constexpr int kCkv = kBlock * kRowCkv;
+  static constexpr int kBytes = kCkv + kBlock * kRowKpe;
+  static constexpr int kNum = kRingBytes / kBytes;
+  // direct-to-LDS loads (1 KiB per wave instruction) per wave per stage
+  static constexpr int kLoads = kBytes / 1024 / 4;
 };
 constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -69,12 +73,17 @@ constexpr float kLn2 = 0.69314718055994530942f;
 // s_waitcnt immediate (gfx9 encoding) that waits for vmcnt <= n only.
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
+// LDS: the stage ring, the compacted pool-block list of the slot range, and
+// for fp8 caches two floats per listed block (latent scale, RoPE / latent
+// scale ratio).
+template <bool FP8>
 struct Lds {
   static constexpr int kList = kRingBytes;
-  static constexpr int kWaveCnt = kList + kMaxSlotsPerSplit * 4;
+  static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
+  static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
   static constexpr int kTotal = kWaveCnt + 16;
 };
-static_assert(Lds::kTotal <= 160 * 1024, "LDS budget");
+static_assert(Lds<true>::kTotal <= 160 * 1024, "LDS budget");
 
 // One direct-to-LDS load per lane: 16 bytes from src to dst + 16 * lane (dst
 // must be wave-uniform; it goes through M0).  Written as asm so that the
@@ -110,9 +119,11 @@ __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 // One k-step of S^T for RG row groups x NT token tiles, as one asm statement:
 // c[rg][tau] += a[tau] . q[rg].  kFirst starts from the literal 0; kLast pads
 // with 24 wait states so the results may be read by VALU code (MFMA results
-// are not interlocked against VALU reads).  Accumulators of consecutive
-// groups are RG*NT - 1 >= 3 independent products apart.
-template <int RG, int NT, bool kFirst, bool kLast>
+// are not interlocked against VALU reads).  kPre leads with 3 wait states, for
+// operands just written by VALU code (VALU writes are not interlocked against
+// MFMA reads either).  Accumulators of consecutive groups are RG*NT - 1 >= 3
+// independent products apart.
+template <int RG, int NT, bool kFirst, bool kLast, bool kPre>
 struct StGroup;
 
 #define MLA_NOPS "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
@@ -146,29 +157,39 @@ struct StGroup;
 #define MLA_OUT14(m) m(c[0][0]), m(c[0][1]), m(c[0][2]), m(c[0][3])
 #define MLA_W(x) "=&v"(x)
 #define MLA_RW(x) "+v"(x)
+#define MLA_PRE "s_nop 2\n\t"
 #define MLA_STGROUP(RG_, NT_, G, OUTS, ...)                                                 \
-  template <bool kLast>                                                                     \
-  struct StGroup<RG_, NT_, true, kLast> {                                                   \
+  template <bool kLast, bool kPre>                                                          \
+  struct StGroup<RG_, NT_, true, kLast, kPre> {                                             \
     static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
                                                const bf16x8_t (&a)[NT_],                    \
                                                const bf16x8_t (&q)[RG_]) {                  \
-      asm(G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                                         \
+      if constexpr (kPre)                                                                   \
+        asm(MLA_PRE G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                               \
+      else                                                                                  \
+        asm(G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                                       \
     }                                                                                       \
   };                                                                                        \
-  template <>                                                                               \
-  struct StGroup<RG_, NT_, false, false> {                                                  \
+  template <bool kPre>                                                                      \
+  struct StGroup<RG_, NT_, false, false, kPre> {                                            \
     static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
                                                const bf16x8_t (&a)[NT_],                    \
                                                const bf16x8_t (&q)[RG_]) {                  \
-      asm(G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                                         \
+      if constexpr (kPre)                                                                   \
+        asm(MLA_PRE G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                               \
+      else                                                                                  \
+        asm(G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                                       \
     }                                                                                       \
   };                                                                                        \
-  template <>                                                                               \
-  struct StGroup<RG_, NT_, false, true> {                                                   \
+  template <bool kPre>                                                                      \
+  struct StGroup<RG_, NT_, false, true, kPre> {                                             \
     static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
                                                const bf16x8_t (&a)[NT_],                    \
                                                const bf16x8_t (&q)[RG_]) {                  \
-      asm(G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                                \
+      if constexpr (kPre)                                                                   \
+        asm(MLA_PRE G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                      \
+      else                                                                                  \
+        asm(G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                              \
     }                                                                                       \
   };
 MLA_STGROUP(2, 4, MLA_G24, MLA_OUT24, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]))
@@ -182,6 +203,7 @@ MLA_STGROUP(1, 4, MLA_G14, MLA_OUT14, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
 #undef MLA_OUT22
 #undef MLA_OUT14
 #undef MLA_NOPS
+#undef MLA_PRE
 #undef MLA_MFMA
 
 // x * s for an accumulator tile that lives in the accumulation registers.
@@ -193,6 +215,16 @@ __device__ __forceinline__ f32x4_t scale_acc(f32x4_t x, float s) {
   x *= s;
   asm volatile("" : "+a"(x));
   return x;
+}
+
+// x *= s in the registers x already occupies.
+__device__ __forceinline__ void scale_inplace(f32x4_t& x, float s) {
+  float x0 = x[0], x1 = x[1], x2 = x[2], x3 = x[3];
+  asm volatile("v_mul_f32 %0, %0, %4\n\tv_mul_f32 %1, %1, %4\n\tv_mul_f32 %2, %2, %4\n\t"
+               "v_mul_f32 %3, %3, %4"
+               : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3)
+               : "v"(s));
+  x = f32x4_t{x0, x1, x2, x3};
 }
 
 __device__ __forceinline__ float xor_max(float v) {
@@ -217,38 +249,63 @@ __device__ __forceinline__ i16x4_t lds_tr16(const LDS uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS i16x4_t*)p);
 }
 
-// Issue the direct-to-LDS loads of tokens part*TOK .. part*TOK+TOK-1 of pool
-// block b into a stage: wave w loads latent rows w*TOK/4 .. (w+1)*TOK/4-1 of
-// the stage (1 KiB each, chunk c placed in slot c ^ (t & 15)) and 1 KiB
-// groups of 8 RoPE rows w*TOK/32 .. (w+1)*TOK/32-1.
-template <int TOK>
-__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, int part,
-                                            LDS uint8_t* buf, int wave, int lane_in) {
+__device__ __forceinline__ int lds_opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Swizzle key of token t (0..63) in an fp8 latent stage: 16-byte chunk c of
+// the token's 512-byte row sits in slot c ^ fp8_key(t).
+__device__ __forceinline__ int fp8_key(int t) { return (t & 15) ^ ((t & 16) >> 1); }
+
+// Issue the direct-to-LDS loads of pool block b into a stage.
+//   bf16: wave w loads latent rows 16w .. 16w+15 (1 KiB each, chunk c in slot
+//         c ^ (t & 15)) and RoPE rows 16w .. 16w+15 (two 1 KiB groups of 8
+//         rows, chunk c in slot c ^ ((t >> 1) & 7)).
+//   fp8:  wave w loads latent rows 16w .. 16w+15 (two 512-byte rows per
+//         1 KiB load, chunk c in slot c ^ fp8_key(t)) and RoPE rows
+//         16w .. 16w+15 (64 bytes each, chunk c in slot c ^ ((t >> 2) & 3)).
+template <bool FP8>
+__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, LDS uint8_t* buf,
+                                            int wave, int lane_in) {
+  using St = Stage<FP8>;
   // Recompute the per-lane source offsets at every issue instead of letting
   // them be hoisted out of the main loop: registers are scarce there.
   int lane;
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
-  const int64_t tok0 = b * kBlock + part * TOK;
-  const uint8_t* ckv = p.ckv + tok0 * (kDLat * 2);
+  const uint8_t* ckv = p.ckv + b * St::kCkv;
+  const uint8_t* kpe = p.kpe + b * (kBlock * St::kRowKpe);
+  if constexpr (!FP8) {
 #pragma unroll
-  for (int j = 0; j < TOK / 4; ++j) {
-    const int t = wave * (TOK / 4) + j;
-    dma16(ckv + t * (kDLat * 2) + ((lane ^ (t & 15)) << 4), buf + t * (kDLat * 2));
-  }
-  const uint8_t* kpe = p.kpe + tok0 * (kDPe * 2);
+    for (int j = 0; j < 16; ++j) {
+      const int t = wave * 16 + j;
+      dma16(ckv + t * St::kRowCkv + ((lane ^ (t & 15)) << 4), buf + t * 1024);
+    }
 #pragma unroll
-  for (int j = 0; j < TOK / 32; ++j) {
-    const int k = wave * (TOK / 32) + j;  // 1 KiB = RoPE rows 8k .. 8k+7
-    const int t = 8 * k + (lane >> 3);
-    const int c = (lane & 7) ^ ((t >> 1) & 7);
-    dma16(kpe + t * (kDPe * 2) + (c << 4), buf + Stage<TOK>::kCkv + k * 1024);
+    for (int j = 0; j < 2; ++j) {
+      const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
+      const int t = 8 * k + (lane >> 3);
+      const int c = (lane & 7) ^ ((t >> 1) & 7);
+      dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + k * 1024);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = wave * 8 + j;  // 1 KiB = latent rows 2k, 2k+1
+      const int t = 2 * k + (lane >> 5);
+      const int c = (lane & 31) ^ fp8_key(t);
+      dma16(ckv + t * St::kRowCkv + (c << 4), buf + k * 1024);
+    }
+    const int t = wave * 16 + (lane >> 2);  // 1 KiB = RoPE rows 16w .. 16w+15
+    const int c = (lane & 3) ^ ((t >> 2) & 3);
+    dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + wave * 1024);
   }
 }
 
 // Wait until at most `stages` later stages of this wave's loads are in flight.
-template <int TOK>
+template <bool FP8>
 __device__ __forceinline__ void wait_stages(int stages) {
-  constexpr int L = Stage<TOK>::kLoads;
+  constexpr int L = Stage<FP8>::kLoads;
   if (stages >= 2)
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * L));
   else if (stages == 1)
@@ -257,15 +314,29 @@ __device__ __forceinline__ void wait_stages(int stages) {
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 }
 
+// Two e4m3 codes (bytes 2*HI, 2*HI+1 of w) -> two bf16, exactly (every e4m3
+// value is a bf16 value; the conversion's own scale is 1).
+template <bool HI>
+__device__ __forceinline__ uint32_t e4m3x2_bf16(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
+// Eight e4m3 codes (two dwords, byte order) -> eight bf16 in the same order.
+__device__ __forceinline__ bf16x8_t e4m3x8_bf16(uint32_t w0, uint32_t w1) {
+  return __builtin_bit_cast(bf16x8_t, u32x4_t{e4m3x2_bf16<false>(w0), e4m3x2_bf16<true>(w0),
+                                              e4m3x2_bf16<false>(w1), e4m3x2_bf16<true>(w1)});
+}
+
 // RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
-// of the row tile (64*RG rows) over all 512 latent columns.
-template <int RG, int TOK>
+// of the row tile (64*RG rows) over all 512 latent columns.  FP8 selects e4m3
+// cache pools with per-block scales.
+template <int RG, bool FP8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void partial_bf16_kernel(const PartialParams p) {
-  using St = Stage<TOK>;
-  constexpr int kTau4 = TOK / 16;  // 16-token tiles per stage
-  constexpr int kKSteps = TOK / 32;  // 32-token PV k-steps per stage
-  using L = Lds;
+void partial_kernel(const PartialParams p) {
+  using St = Stage<FP8>;
+  using L = Lds<FP8>;
+  constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
+  constexpr int kKSteps = kBlock / 32;  // 32-token PV k-steps per block
   constexpr int kRowsWg = 64 * RG;
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
   LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
@@ -286,6 +357,7 @@ void partial_bf16_kernel(const PartialParams p) {
 
   // ---- compact the valid selected blocks of the slot range (slot order kept)
   LDS int* list = (LDS int*)(smem + L::kList);
+  LDS float* scales = (LDS float*)(smem + L::kScales);
   LDS int* wave_cnt = (LDS int*)(smem + L::kWaveCnt);
   int n_valid = 0;
   for (int base = 0; base < nslots; base += 256) {
@@ -309,12 +381,21 @@ void partial_bf16_kernel(const PartialParams p) {
       off += (w < wave) ? c : 0;
       total += c;
     }
-    if (b >= 0) list[off + before] = b;
+    if (b >= 0) {
+      list[off + before] = b;
+      if constexpr (FP8) {
+        const float sc = p.ckv_scale[b];
+        scales[2 * (off + before)] = sc;
+        scales[2 * (off + before) + 1] = p.kpe_scale[b] / sc;
+      }
+    }
     n_valid += total;
     __syncthreads();
   }
 
-  // ---- this wave's query rows as MFMA B operands, held for the whole kernel
+  // ---- this wave's query rows as MFMA B operands, held for the whole kernel:
+  // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
+  // dims 32ks' + 8g .. +7 (ks' = the step within its part).
   const int row_wg0 = rt * kRowsWg;
   bf16x8_t qb[RG][18];
 #pragma unroll
@@ -349,74 +430,136 @@ void partial_bf16_kernel(const PartialParams p) {
     l_run[rg] = 0.f;
   }
 
-  // ---- main loop over stages: up to St::kNum - 1 stages stream in while one
-  // is computed
-  const int n_stage = n_valid * St::kPerBlock;
-  for (int h = 0; h < n_stage && h < St::kNum - 1; ++h)
-    issue_stage<TOK>(p, list[h / St::kPerBlock], h % St::kPerBlock, smem + h * St::kBytes, wave,
-                     lane);
-  for (int h = 0; h < n_stage; ++h) {
-    wait_stages<TOK>(min(n_stage - 1 - h, St::kNum - 2));
-    lds_barrier();  // stage h is in LDS for every wave; every wave is done with stage h-1
+  // ---- main loop over the listed blocks: up to St::kNum - 1 blocks stream in
+  // while one is computed
+  for (int h = 0; h < n_valid && h < St::kNum - 1; ++h)
+    issue_stage<FP8>(p, list[h], smem + h * St::kBytes, wave, lane);
+  for (int h = 0; h < n_valid; ++h) {
+    wait_stages<FP8>(min(n_valid - 1 - h, St::kNum - 2));
+    lds_barrier();  // block h is in LDS for every wave; every wave is done with block h-1
     {
       // All of the next stage's loads at once: spreading them between the
       // products measured slower (each load holds the issuing wave until the
       // shared address unit takes it, and the stage's LDS reads then compete
       // with the incoming writes).
       const int hn = h + St::kNum - 1;
-      if (hn < n_stage)
-        issue_stage<TOK>(p, list[hn / St::kPerBlock], hn % St::kPerBlock,
-                         smem + (hn % St::kNum) * St::kBytes, wave, lane);
+      if (hn < n_valid) issue_stage<FP8>(p, list[hn], smem + (hn % St::kNum) * St::kBytes, wave, lane);
     }
     const LDS uint8_t* cb = smem + (h % St::kNum) * St::kBytes;
+    // fp8: the block's latent scale and RoPE / latent scale ratio.  The scores
+    // are accumulated as ratio * (q_pe . kpe codes) + q_lat . ckv codes and then
+    // scaled by scale * latent scale; P is scaled by the latent scale for PV.
+    float s_mult = p.scale_log2, v_mult = 1.f, pe_ratio = 1.f;
+    if constexpr (FP8) {
+      v_mult = scales[2 * h];
+      pe_ratio = scales[2 * h + 1];
+      s_mult = p.scale_log2 * v_mult;
+    }
 
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
     // every iteration (a few VALU ops) rather than held in registers across
     // the loop.
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
+    const int ln = lds_opaque(lane);
     const int ln16 = ln & 15, lg = ln >> 4;
 
-    // S^T[token][row], tokens 16*tau + ln16.  Latent chunk 4ks+lg of that token
-    // sits in slot (4ks+lg) ^ ln16, i.e. at key_base ^ ((ks & 3) << 6) plus
-    // (ks >> 2) * 256 within the token's row.
-    const int key_base = ln16 * 1024 + ((lg ^ (ln16 & 3)) << 4) + ((ln16 >> 2) << 6);
-    const int rope_base = St::kCkv + ln16 * 128;
-    // 18 k-steps (2 RoPE, then 16 latent), 4 token tiles each
-    auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
-      if (step < 2) {
-#pragma unroll
-        for (int tau = 0; tau < kTau4; ++tau)
-          a[tau] = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
-      } else {
-        const int ks = step - 2;
-#pragma unroll
-        for (int tau = 0; tau < kTau4; ++tau)
-          a[tau] = lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((ks & 3) << 6)));
-      }
-    };
-    // Software pipeline: the key fragments of step k+2 are requested before
-    // the products of step k (a ring of three fragment sets); the scheduling
-    // fences keep the compiler from regrouping loads next to their use.
+    // S^T[token][row] for tokens 16*tau + ln16: 18 k-steps (2 RoPE, then 16
+    // latent), 4 token tiles each.  Software pipeline: key fragments are
+    // requested about two steps before their products; the scheduling fences
+    // keep the compiler from regrouping loads next to their use.
     f32x4_t sacc[RG][kTau4];
-    bf16x8_t ka[3][kTau4];
-    key_frags(0, ka[0]);
-    key_frags(1, ka[1]);
+    if constexpr (!FP8) {
+      // Latent chunk 4ks+lg of token 16tau+ln16 sits in slot (4ks+lg) ^ ln16,
+      // i.e. at key_base ^ ((ks & 3) << 6) plus (ks >> 2) * 256 within the row.
+      const int key_base = ln16 * 1024 + ((lg ^ (ln16 & 3)) << 4) + ((ln16 >> 2) << 6);
+      const int rope_base = St::kCkv + ln16 * 128;
+      auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
+        if (step < 2) {
 #pragma unroll
-    for (int step = 0; step < 18; ++step) {
-      if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
-      __builtin_amdgcn_sched_barrier(0);
-      const int ks = step < 2 ? 16 + step : step - 2;
-      bf16x8_t q[RG];
+          for (int tau = 0; tau < kTau4; ++tau)
+            a[tau] = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
+        } else {
+          const int ks = step - 2;
 #pragma unroll
-      for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
-      if (step == 0)
-        StGroup<RG, kTau4, true, false>::run(sacc, ka[0], q);
-      else if (step == 17)
-        StGroup<RG, kTau4, false, true>::run(sacc, ka[step % 3], q);
-      else
-        StGroup<RG, kTau4, false, false>::run(sacc, ka[step % 3], q);
-      __builtin_amdgcn_sched_barrier(0);
+          for (int tau = 0; tau < kTau4; ++tau)
+            a[tau] = lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((ks & 3) << 6)));
+        }
+      };
+      bf16x8_t ka[3][kTau4];
+      key_frags(0, ka[0]);
+      key_frags(1, ka[1]);
+#pragma unroll
+      for (int step = 0; step < 18; ++step) {
+        if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
+        __builtin_amdgcn_sched_barrier(0);
+        const int ks = step < 2 ? 16 + step : step - 2;
+        bf16x8_t q[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
+        if (step == 0)
+          StGroup<RG, kTau4, true, false, false>::run(sacc, ka[0], q);
+        else if (step == 17)
+          StGroup<RG, kTau4, false, true, false>::run(sacc, ka[step % 3], q);
+        else
+          StGroup<RG, kTau4, false, false, false>::run(sacc, ka[step % 3], q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      // One 8-byte read per lane and tile per k-step: latent dims 32ks + 8lg
+      // of token t = 16tau + ln16 are half (lg & 1) of chunk 2ks + (lg >> 1),
+      // which sits in slot (2ks + (lg >> 1)) ^ fp8_key(t), fp8_key(t) =
+      // ln16 ^ 8(tau & 1); RoPE dims 32ks + 8lg are half (lg & 1) of chunk
+      // 2ks + (lg >> 1) of the token's 64-byte RoPE row, in slot
+      // chunk ^ ((t >> 2) & 3).
+      const int key_base =
+          ln16 * St::kRowCkv + ((((lg >> 1) ^ ln16)) << 4) + ((lg & 1) << 3);
+      const int rope_base = St::kCkv + ln16 * St::kRowKpe + ((lg & 1) << 3);
+      const int rope_key = (ln16 >> 2) & 3;
+      auto key_raw = [&](int step, i32x2_t (&a)[kTau4]) {
+        if (step < 2) {
+#pragma unroll
+          for (int tau = 0; tau < kTau4; ++tau)
+            a[tau] = *(const LDS i32x2_t*)(cb + rope_base + tau * 16 * St::kRowKpe +
+                                          (((2 * step + (lg >> 1)) ^ rope_key) << 4));
+        } else {
+          const int ks = step - 2;
+#pragma unroll
+          for (int tau = 0; tau < kTau4; ++tau)
+            a[tau] = *(const LDS i32x2_t*)(cb + tau * 16 * St::kRowCkv +
+                                          (key_base ^ (ks << 5) ^ ((tau & 1) << 7)));
+        }
+      };
+      i32x2_t kr[3][kTau4];
+      key_raw(0, kr[0]);
+      key_raw(1, kr[1]);
+#pragma unroll
+      for (int step = 0; step < 18; ++step) {
+        if (step + 2 < 18) key_raw(step + 2, kr[(step + 2) % 3]);
+        __builtin_amdgcn_sched_barrier(0);
+        const int ks = step < 2 ? 16 + step : step - 2;
+        bf16x8_t a[kTau4], q[RG];
+#pragma unroll
+        for (int tau = 0; tau < kTau4; ++tau)
+          a[tau] = e4m3x8_bf16((uint32_t)kr[step % 3][tau][0], (uint32_t)kr[step % 3][tau][1]);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
+        if (step == 0) {
+          StGroup<RG, kTau4, true, false, true>::run(sacc, a, q);
+        } else if (step == 1 || step == 17) {
+          StGroup<RG, kTau4, false, true, true>::run(sacc, a, q);
+        } else {
+          if (step == 2) {
+            // The RoPE part is complete: weight it by its scale relative to
+            // the latent scale, in place (the next group's lead covers this
+            // VALU write of its accumulators).
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+              for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
+          }
+          StGroup<RG, kTau4, false, false, true>::run(sacc, a, q);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     f32x4_t acc[RG][kTau4];
 #pragma unroll
@@ -424,7 +567,7 @@ void partial_bf16_kernel(const PartialParams p) {
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) acc[rg][tau] = sacc[rg][tau];
 
-    // Online softmax over the stage's TOK tokens (exp2 domain).  Lane (n16, g)
+    // Online softmax over the block's 64 tokens (exp2 domain).  Lane (n16, g)
     // holds row n16 of each row group and tokens 16*tau + 4g + i.
     bool need_any = false;
     float bmax[RG];
@@ -433,7 +576,7 @@ void partial_bf16_kernel(const PartialParams p) {
       float bm = -INFINITY;
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) {
-        acc[rg][tau] *= p.scale_log2;
+        acc[rg][tau] *= s_mult;
 #pragma unroll
         for (int k = 0; k < 4; ++k) bm = fmaxf(bm, acc[rg][tau][k]);
       }
@@ -455,7 +598,9 @@ void partial_bf16_kernel(const PartialParams p) {
         }
       }
     }
-    // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}
+    // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}.
+    // The row sum takes the unrounded fp32 weights; the PV operand is rounded
+    // to bf16 (after the latent scale, for fp8).
     bf16x8_t pb[RG][kKSteps];
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
@@ -466,46 +611,77 @@ void partial_bf16_kernel(const PartialParams p) {
         for (int k = 0; k < 4; ++k) {
           const float e = __builtin_amdgcn_exp2f(acc[rg][tau][k] - m_run[rg]);
           ps += e;
-          pb[rg][tau >> 1][(tau & 1) * 4 + k] = (__bf16)e;
+          pb[rg][tau >> 1][(tau & 1) * 4 + k] = (__bf16)(FP8 ? e * v_mult : e);
         }
       l_run[rg] += ps;
     }
 
-    // O^T[dim][row] += V^T . P^T.  Value rows for lane (g, r4, q4): token
-    // 32ps + 16hh + 4g + r4 (= 32ps + 16hh + (lane >> 2)), latent columns
-    // 16dt + 4q4 .. +3, i.e. chunk 2dt + (q4 >> 1) of a row whose swizzle key is
-    // x = lane >> 2.  The slot (2dt + (q4>>1)) ^ x splits into a per-lane part
-    // and (dt & 7) << 1 XORed into bits 1..3, plus the 16-chunk group dt >> 3.
-    int lv = lane;
-    asm volatile("" : "+v"(lv));
-    const int x = lv >> 2, q4 = lv & 3;
-    const int tr_base = x * 1024 + ((2 * (x >> 1) + ((q4 >> 1) ^ (x & 1))) << 4) + ((q4 & 1) << 3);
-    auto tr_off = [&](int ps, int hh, int dt) {
-      return (tr_base ^ ((dt & 7) << 5)) + (dt >> 3) * 256 + ps * 32768 + hh * 16384;
-    };
-    // kKSteps x 32 value fragments (k-steps x column tiles) in a software
-    // pipeline kPvAhead fragments deep.
+    // O^T[dim][row] += V^T . P^T over 2 k-steps x 32 column tiles, in a
+    // software pipeline kPvAhead fragments deep.  The value fragment of k-step
+    // ps and column tile dt must list, for lane (g, c), column 16dt + c of the
+    // tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}, in that order.
     constexpr int kPvAhead = 8;
     constexpr int kFrags = 32 * kKSteps;
-    auto v_frag = [&](int f) {
-      const int ps = f >> 5, dt = f & 31;
-      const i16x4_t lo = lds_tr16(cb + tr_off(ps, 0, dt));
-      const i16x4_t hi = lds_tr16(cb + tr_off(ps, 1, dt));
-      return __builtin_bit_cast(bf16x8_t,
-                                i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-    };
-    bf16x8_t va[kPvAhead + 1];
+    const int lv = lds_opaque(lane);
+    if constexpr (!FP8) {
+      // Transposing 16-bit reads of 4 tokens x 4 columns per lane group of 4:
+      // lane (x = lane >> 2, q4 = lane & 3) supplies token 32ps + 16hh + x,
+      // columns 16dt + 4q4 .. +3 = chunk 2dt + (q4 >> 1); that chunk's slot
+      // (2dt + (q4>>1)) ^ x splits into a per-lane part and (dt & 7) << 1
+      // XORed into bits 1..3, plus the 16-chunk group dt >> 3.
+      const int x = lv >> 2, q4 = lv & 3;
+      const int tr_base =
+          x * 1024 + ((2 * (x >> 1) + ((q4 >> 1) ^ (x & 1))) << 4) + ((q4 & 1) << 3);
+      auto tr_off = [&](int ps, int hh, int dt) {
+        return (tr_base ^ ((dt & 7) << 5)) + (dt >> 3) * 256 + ps * 32768 + hh * 16384;
+      };
+      auto v_frag = [&](int f) {
+        const int ps = f >> 5, dt = f & 31;
+        const i16x4_t lo = lds_tr16(cb + tr_off(ps, 0, dt));
+        const i16x4_t hi = lds_tr16(cb + tr_off(ps, 1, dt));
+        return __builtin_bit_cast(bf16x8_t,
+                                  i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+      };
+      bf16x8_t va[kPvAhead + 1];
 #pragma unroll
-    for (int f = 0; f < kPvAhead; ++f) va[f] = v_frag(f);
+      for (int f = 0; f < kPvAhead; ++f) va[f] = v_frag(f);
 #pragma unroll
-    for (int f = 0; f < kFrags; ++f) {
-      if (f + kPvAhead < kFrags) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
-      __builtin_amdgcn_sched_barrier(0);
-      const int ps = f >> 5, dt = f & 31;
+      for (int f = 0; f < kFrags; ++f) {
+        if (f + kPvAhead < kFrags) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
+        __builtin_amdgcn_sched_barrier(0);
+        const int ps = f >> 5, dt = f & 31;
 #pragma unroll
-      for (int rg = 0; rg < RG; ++rg)
-        O[dt][rg] = mfma(va[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
-      __builtin_amdgcn_sched_barrier(0);
+        for (int rg = 0; rg < RG; ++rg)
+          O[dt][rg] = mfma(va[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      // One transposing 8-bit read per fragment: in each 16-lane group, lane
+      // 2j + q supplies 8 columns (16dt + 8q ..) of the fragment's j-th token
+      // and lane c receives column 16dt + c of the 8 tokens.  Token
+      // 32ps + 16(j >> 2) + 4g + (j & 3) has swizzle key 4g + (j & 3) ^ 8(j >> 2).
+      const int c = lv & 15, j = c >> 1, gq = lv >> 4;
+      const int key = (4 * gq + (j & 3)) ^ ((j >> 2) << 3);
+      const int tr_base = (16 * (j >> 2) + 4 * gq + (j & 3)) * St::kRowCkv + (key << 4) + ((c & 1) << 3);
+      auto v_raw = [&](int f) {
+        const int ps = f >> 5, dt = f & 31;
+        return __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (LDS i32x2_t*)(cb + ps * 32 * St::kRowCkv + (tr_base ^ (dt << 4))));
+      };
+      i32x2_t vr[kPvAhead + 1];
+#pragma unroll
+      for (int f = 0; f < kPvAhead; ++f) vr[f] = v_raw(f);
+#pragma unroll
+      for (int f = 0; f < kFrags; ++f) {
+        if (f + kPvAhead < kFrags) vr[(f + kPvAhead) % (kPvAhead + 1)] = v_raw(f + kPvAhead);
+        __builtin_amdgcn_sched_barrier(0);
+        const int ps = f >> 5, dt = f & 31;
+        const i32x2_t w = vr[f % (kPvAhead + 1)];
+        const bf16x8_t va = e4m3x8_bf16((uint32_t)w[0], (uint32_t)w[1]);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(va, pb[rg][ps], O[dt][rg]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
 
@@ -536,18 +712,20 @@ void partial_bf16_kernel(const PartialParams p) {
 
 }  // namespace
 
-#ifndef MLA_STAGE_TOKENS
-#define MLA_STAGE_TOKENS 64
-#endif
-
 hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s) {
-  if (fp8) return hipErrorNotSupported;
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (row_groups == 2)
-    hipLaunchKernelGGL((partial_bf16_kernel<2, MLA_STAGE_TOKENS>), dim3(grid), dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((partial_bf16_kernel<1, 64>), dim3(grid), dim3(256), 0, s, p);
+  if (fp8) {
+    if (row_groups == 2)
+      hipLaunchKernelGGL((partial_kernel<2, true>), dim3(grid), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((partial_kernel<1, true>), dim3(grid), dim3(256), 0, s, p);
+  } else {
+    if (row_groups == 2)
+      hipLaunchKernelGGL((partial_kernel<2, false>), dim3(grid), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((partial_kernel<1, false>), dim3(grid), dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 

@@ -97,22 +97,18 @@ def quantize_e4m3fn(y: np.ndarray) -> np.ndarray:
     y = np.asarray(y, dtype=np.float64)
     sign = np.signbit(y).astype(np.uint8) << np.uint8(7)
     a = np.minimum(np.abs(y), E4M3_MAX)
-    # exponent of the binade of a, at least the smallest normal exponent -6
-    _, ex = np.frexp(a)  # a = f * 2^ex, f in [0.5, 1)
-    e = np.maximum(ex - 1, -6)
-    quantum = np.ldexp(1.0, e - 3)
-    q = np.rint(a / quantum) * quantum  # rint: ties to even
-    q = np.minimum(q, E4M3_MAX)
-    # encode q
-    _, ex2 = np.frexp(q)
-    e2 = ex2 - 1
-    normal = q >= 2.0 ** -6
-    e_field = np.where(normal, e2 + 7, 0)
-    m_norm = np.where(normal, np.ldexp(q, -e2) * 8.0 - 8.0, 0.0)
-    m_sub = np.where(normal, 0.0, q * 512.0)
-    m_field = np.where(normal, m_norm, m_sub)
-    code = (e_field.astype(np.int64) << 3) | np.rint(m_field).astype(np.int64)
-    return (code.astype(np.uint8) | sign).astype(np.uint8)
+    # Normal range [2^-6, 448]: round the float64 significand to 3 bits, ties
+    # to even, on the bit pattern (a carry moves into the exponent); then
+    # rebias the exponent from 1023 to 7.
+    b = a.view(np.uint64)
+    lsb = (b >> np.uint64(49)) & np.uint64(1)
+    r = (b + np.uint64((1 << 48) - 1) + lsb) >> np.uint64(49)
+    code_n = r.astype(np.int64) - ((1023 - 7) << 3)
+    # Subnormal range: multiples of 2^-9 (rint ties to even; 8 * 2^-9 is the
+    # smallest normal, code 8).
+    code_s = np.rint(a * 512.0).astype(np.int64)
+    code = np.where(a < 2.0 ** -6, code_s, code_n)
+    return code.astype(np.uint8) | sign
 
 
 def quantize_blocks_e4m3fn(bits: np.ndarray):
@@ -125,7 +121,7 @@ def quantize_blocks_e4m3fn(bits: np.ndarray):
     P = bits.shape[0]
     codes = np.empty(bits.shape, np.uint8)
     scales = np.empty(P, np.float32)
-    step = 256
+    step = 16  # small chunks: temporaries of a few MB are reused from the heap
 
     def work(lo):
         hi = min(P, lo + step)
