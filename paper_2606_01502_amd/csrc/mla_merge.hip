@@ -7,9 +7,11 @@
 // A part with lse = -inf is skipped (its o is never read, so a NaN there
 // cannot leak); no live part gives out = 0, lse = -inf.
 //
-// HBM-bound elementwise work: 128 lanes per 512-wide row, each lane moving
-// 16-byte vectors; every lane of a row recomputes the row's weights from the
-// n lse values (a few exp per lane against n 16-byte loads).
+// HBM-bound: one wave per row.  The wave reads the row's part lse values
+// lane-parallel (lane j holds part j), reduces max and sum across the wave,
+// and then visits only the live parts, eight at a time, with each lane moving
+// two 16-byte vectors per part (columns 4*lane and 256 + 4*lane), so that
+// sixteen loads per lane are in flight instead of one part at a time.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -21,68 +23,113 @@ namespace {
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kRowsPerBlock = kThreads / 128;  // 2 rows of 512 floats per workgroup
+constexpr int kRowsPerBlock = kThreads / 64;  // one wave per row
+constexpr int kBatch = 8;                    // parts in flight per wave
 
-// Merged lse of one row's parts; -inf when no part is live.
-template <typename LseAt>
-__device__ __forceinline__ float merged_lse(int n, LseAt lse_at) {
-  float m = -INFINITY;
-  for (int j = 0; j < n; ++j) m = fmaxf(m, lse_at(j));
-  if (m == -INFINITY) return -INFINITY;
-  float s = 0.f;
-  for (int j = 0; j < n; ++j) {
-    const float l = lse_at(j);
-    if (l != -INFINITY) s += __expf(l - m);
-  }
-  return m + __logf(s);
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
 }
 
-// sum over live parts of exp(lse_j - lse) * o_j[col .. col+3]
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Merge n parts of one row.  lse_at(j): part j's lse; row_at(j): part j's
+// 512 floats.  Writes the 512 outputs at out and returns the merged lse.
 template <typename LseAt, typename RowAt>
-__device__ __forceinline__ f32x4_t merged_row(int n, float lse, LseAt lse_at, RowAt row_at) {
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  if (lse == -INFINITY) return acc;
-  for (int j = 0; j < n; ++j) {
-    const float l = lse_at(j);
-    if (l != -INFINITY) acc += __expf(l - lse) * *row_at(j);
+__device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, float* out,
+                                           int lane) {
+  float m = -INFINITY;
+  for (int j0 = 0; j0 < n; j0 += 64) {
+    const int j = j0 + lane;
+    if (j < n) m = fmaxf(m, lse_at(j));
   }
-  return acc;
+  m = wave_max(m);
+  f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  float lse = -INFINITY;
+  if (m != -INFINITY) {
+    float s = 0.f;
+    for (int j0 = 0; j0 < n; j0 += 64) {
+      const int j = j0 + lane;
+      const float l = j < n ? lse_at(j) : -INFINITY;
+      if (l != -INFINITY) s += __expf(l - m);
+    }
+    lse = m + __logf(wave_sum(s));
+    for (int j0 = 0; j0 < n; j0 += 64) {
+      const int j = j0 + lane;
+      const float l = j < n ? lse_at(j) : -INFINITY;
+      const float w = l != -INFINITY ? __expf(l - lse) : 0.f;
+      uint64_t live = __ballot(l != -INFINITY);
+      while (live) {
+        int idx[kBatch];
+        int cnt = 0;
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+          idx[k] = live ? __builtin_ctzll(live) : idx[0];
+          if (live) {
+            live &= live - 1;
+            ++cnt;
+          }
+        }
+        f32x4_t v0[kBatch], v1[kBatch];
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+          if (k < cnt) {
+            const float* r = row_at(j0 + idx[k]);
+            v0[k] = *(const f32x4_t*)(r + 4 * lane);
+            v1[k] = *(const f32x4_t*)(r + 256 + 4 * lane);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+          if (k < cnt) {
+            const float wk = __shfl(w, idx[k]);
+            acc0 += wk * v0[k];
+            acc1 += wk * v1[k];
+          }
+        }
+      }
+    }
+  }
+  *(f32x4_t*)(out + 4 * lane) = acc0;
+  *(f32x4_t*)(out + 256 + 4 * lane) = acc1;
+  return lse;
 }
 
 __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
   const int n_rows = p.B * p.Mq * p.H;
-  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 7);
+  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (row >= n_rows) return;
-  const int col = (threadIdx.x & 127) * 4;
+  const int lane = threadIdx.x & 63;
   const int b = row / (p.Mq * p.H);
   const int rem = row - b * (p.Mq * p.H);
   const int i = rem / p.H, h = rem - (rem / p.H) * p.H;
   const int64_t lo = b * p.l_s0 + i * p.l_s1 + h * p.l_s2;
-  const int64_t oo = b * p.o_s0 + i * p.o_s1 + h * p.o_s2 + col;
-  auto lse_at = [&](int j) { return p.lse[j][lo]; };
-  const float lse = merged_lse(p.n_parts, lse_at);
-  const f32x4_t acc = merged_row(p.n_parts, lse, lse_at,
-                                 [&](int j) { return (const f32x4_t*)(p.o[j] + oo); });
-  *(f32x4_t*)(p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2 + col) = acc;
-  if (p.out_lse && col == 0) p.out_lse[b * p.ol_s0 + i * p.ol_s1 + h * p.ol_s2] = lse;
+  const int64_t oo = b * p.o_s0 + i * p.o_s1 + h * p.o_s2;
+  const float lse = merge_row(
+      p.n_parts, [&](int j) { return p.lse[j][lo]; }, [&](int j) { return p.o[j] + oo; },
+      p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
+  if (p.out_lse && lane == 0) p.out_lse[b * p.ol_s0 + i * p.ol_s1 + h * p.ol_s2] = lse;
 }
 
 __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineParams p) {
   const int n_rows = p.R * p.rows;
-  const int grow = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 7);
+  const int grow = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (grow >= n_rows) return;
-  const int col = (threadIdx.x & 127) * 4;
+  const int lane = threadIdx.x & 63;
   const int r = grow / p.rows;
   const int row = grow - r * p.rows;
   const int64_t base = (int64_t)r * p.S * p.rows + row;  // split j of (r, row) at base + j*rows
-  auto lse_at = [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; };
-  const float lse = merged_lse(p.S, lse_at);
-  const f32x4_t acc = merged_row(p.S, lse, lse_at, [&](int j) {
-    return (const f32x4_t*)(p.ws_o + (base + (int64_t)j * p.rows) * kDLat + col);
-  });
   const int i = row / p.H, h = row - (row / p.H) * p.H;
-  *(f32x4_t*)(p.out + r * p.out_s0 + i * p.out_s1 + h * p.out_s2 + col) = acc;
-  if (col == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2] = lse;
+  const float lse = merge_row(
+      p.S, [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; },
+      [&](int j) { return p.ws_o + (base + (int64_t)j * p.rows) * kDLat; },
+      p.out + r * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
+  if (lane == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2] = lse;
 }
 
 }  // namespace

@@ -27,11 +27,9 @@
 //            caller's buffers or, under split-K, to a workspace that the
 //            combine kernel reduces with the merge algebra (Section 3.3).
 //
-// LDS swizzles (token t of the block, 16-byte chunk c of its row): latent
-// chunk c lives in slot c ^ (t & 15); RoPE chunk c in slot c ^ ((t >> 1) & 7).
-// The b128 key reads (16 consecutive tokens, one chunk) and the transposing
-// value reads (16 consecutive tokens, two chunks) then cover every LDS bank at
-// the minimum number of cycles.
+// LDS swizzles (token t of the block, 16-byte chunk c of its row) keep every
+// read pattern free of bank conflicts; they are described with bf16_key and
+// fp8_key below.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -254,20 +252,36 @@ __device__ __forceinline__ int lds_opaque(int v) {
   return v;
 }
 
+// LDS bank rules on gfx950 (measured with the bank-conflict counter): 64
+// banks of 4 bytes.  An 8-byte read serves 32 consecutive lanes per cycle; a
+// transposing 8-byte read also serves 32 consecutive lanes but claims banks in
+// 32-byte granules; a 16-byte read serves 16 lanes per cycle, the four 4-lane
+// quads of a half-wave whose quad index (lane >> 2 & 7) has the same parity.
+//
+// Swizzle key of token t in a bf16 latent stage: 16-byte chunk c of the
+// token's 1 KiB row sits in slot c ^ bf16_key(t).  With the key t & 15 the key
+// reads (token t & 15 and chunk group lane >> 4 by lane) are conflict free
+// and the transposing value reads are 2-way conflicted; keys that make both
+// conflict free exist (for instance ((t & 3) << 1) | (t >> 2 & 1) |
+// ((t >> 2 ^ t >> 3) & 1) << 3) but measured slower in this kernel, whose
+// LDS traffic is not the limit.
+__device__ __forceinline__ int bf16_key(int t) { return t & 15; }
+
 // Swizzle key of token t (0..63) in an fp8 latent stage: 16-byte chunk c of
 // the token's 512-byte row sits in slot c ^ fp8_key(t).
 __device__ __forceinline__ int fp8_key(int t) { return (t & 15) ^ ((t & 16) >> 1); }
 
-// Issue the direct-to-LDS loads of pool block b into a stage.
-//   bf16: wave w loads latent rows 16w .. 16w+15 (1 KiB each, chunk c in slot
-//         c ^ (t & 15)) and RoPE rows 16w .. 16w+15 (two 1 KiB groups of 8
-//         rows, chunk c in slot c ^ ((t >> 1) & 7)).
-//   fp8:  wave w loads latent rows 16w .. 16w+15 (two 512-byte rows per
-//         1 KiB load, chunk c in slot c ^ fp8_key(t)) and RoPE rows
-//         16w .. 16w+15 (64 bytes each, chunk c in slot c ^ ((t >> 2) & 3)).
+// Issue direct-to-LDS loads j0 .. j1-1 (of Stage<FP8>::kLoads per wave) of
+// pool block b into a stage.
+//   bf16: load j < 16 is latent row 16w + j (1 KiB; chunk c in slot
+//         c ^ bf16_key(t)); loads 16, 17 are RoPE rows 16w .. 16w+7 and
+//         16w+8 .. 16w+15 (chunk c in slot c ^ ((t >> 1) & 7)).
+//   fp8:  load j < 8 is latent rows 16w + 2j, 16w + 2j + 1 (512 bytes each;
+//         chunk c in slot c ^ fp8_key(t)); load 8 is RoPE rows 16w .. 16w+15
+//         (64 bytes each; chunk c in slot c ^ ((t >> 2) & 3)).
 template <bool FP8>
-__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, LDS uint8_t* buf,
-                                            int wave, int lane_in) {
+__device__ __forceinline__ void issue_part(const PartialParams& p, int64_t b, LDS uint8_t* buf,
+                                           int wave, int lane_in, int j0, int j1) {
   using St = Stage<FP8>;
   // Recompute the per-lane source offsets at every issue instead of letting
   // them be hoisted out of the main loop: registers are scarce there.
@@ -275,30 +289,30 @@ __device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, L
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
   const uint8_t* ckv = p.ckv + b * St::kCkv;
   const uint8_t* kpe = p.kpe + b * (kBlock * St::kRowKpe);
-  if constexpr (!FP8) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int t = wave * 16 + j;
-      dma16(ckv + t * St::kRowCkv + ((lane ^ (t & 15)) << 4), buf + t * 1024);
+  for (int j = j0; j < j1; ++j) {
+    if constexpr (!FP8) {
+      if (j < 16) {
+        const int t = wave * 16 + j;
+        dma16(ckv + t * St::kRowCkv + ((lane ^ bf16_key(t)) << 4), buf + t * 1024);
+      } else {
+        const int k = wave * 2 + (j - 16);  // 1 KiB = RoPE rows 8k .. 8k+7
+        const int t = 8 * k + (lane >> 3);
+        const int c = (lane & 7) ^ ((t >> 1) & 7);
+        dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + k * 1024);
+      }
+    } else {
+      if (j < 8) {
+        const int k = wave * 8 + j;  // 1 KiB = latent rows 2k, 2k+1
+        const int t = 2 * k + (lane >> 5);
+        const int c = (lane & 31) ^ fp8_key(t);
+        dma16(ckv + t * St::kRowCkv + (c << 4), buf + k * 1024);
+      } else {
+        const int t = wave * 16 + (lane >> 2);  // 1 KiB = RoPE rows 16w .. 16w+15
+        const int c = (lane & 3) ^ ((t >> 2) & 3);
+        dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + wave * 1024);
+      }
     }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
-      const int t = 8 * k + (lane >> 3);
-      const int c = (lane & 7) ^ ((t >> 1) & 7);
-      dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + k * 1024);
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = wave * 8 + j;  // 1 KiB = latent rows 2k, 2k+1
-      const int t = 2 * k + (lane >> 5);
-      const int c = (lane & 31) ^ fp8_key(t);
-      dma16(ckv + t * St::kRowCkv + (c << 4), buf + k * 1024);
-    }
-    const int t = wave * 16 + (lane >> 2);  // 1 KiB = RoPE rows 16w .. 16w+15
-    const int c = (lane & 3) ^ ((t >> 2) & 3);
-    dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + wave * 1024);
   }
 }
 
@@ -373,7 +387,7 @@ void partial_kernel(const PartialParams p) {
     const uint64_t m = __ballot(b >= 0);
     const int before = __popcll(m & ((1ull << lane) - 1ull));
     if (lane == 0) wave_cnt[wave] = __popcll(m);
-    __syncthreads();
+    lds_barrier();
     int off = n_valid, total = 0;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -390,8 +404,13 @@ void partial_kernel(const PartialParams p) {
       }
     }
     n_valid += total;
-    __syncthreads();
+    lds_barrier();
   }
+
+  // ---- the first stages' loads go out before the query rows, so that their
+  // latencies overlap
+  for (int h = 0; h < n_valid && h < St::kNum - 1; ++h)
+    issue_part<FP8>(p, list[h], smem + h * St::kBytes, wave, lane, 0, St::kLoads);
 
   // ---- this wave's query rows as MFMA B operands, held for the whole kernel:
   // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
@@ -414,8 +433,9 @@ void partial_kernel(const PartialParams p) {
       for (int ks = 0; ks < 18; ++ks) qb[rg][ks] = bf16x8_t{};
     }
   }
-  // Q is resident before the first prefetch is issued, so that the only
-  // vector-memory operation in flight inside the main loop is the prefetch.
+  // Q (and with it the first stages) is resident before the main loop, so
+  // that the only vector-memory operations in flight inside the loop are the
+  // prefetches the loop issues itself.
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
   f32x4_t O[32][RG];
@@ -432,8 +452,6 @@ void partial_kernel(const PartialParams p) {
 
   // ---- main loop over the listed blocks: up to St::kNum - 1 blocks stream in
   // while one is computed
-  for (int h = 0; h < n_valid && h < St::kNum - 1; ++h)
-    issue_stage<FP8>(p, list[h], smem + h * St::kBytes, wave, lane);
   for (int h = 0; h < n_valid; ++h) {
     wait_stages<FP8>(min(n_valid - 1 - h, St::kNum - 2));
     lds_barrier();  // block h is in LDS for every wave; every wave is done with block h-1
@@ -443,7 +461,9 @@ void partial_kernel(const PartialParams p) {
       // shared address unit takes it, and the stage's LDS reads then compete
       // with the incoming writes).
       const int hn = h + St::kNum - 1;
-      if (hn < n_valid) issue_stage<FP8>(p, list[hn], smem + (hn % St::kNum) * St::kBytes, wave, lane);
+      if (hn < n_valid)
+        issue_part<FP8>(p, list[hn], smem + (hn % St::kNum) * St::kBytes, wave, lane, 0,
+                        St::kLoads);
     }
     const LDS uint8_t* cb = smem + (h % St::kNum) * St::kBytes;
     // fp8: the block's latent scale and RoPE / latent scale ratio.  The scores
@@ -468,9 +488,9 @@ void partial_kernel(const PartialParams p) {
     // keep the compiler from regrouping loads next to their use.
     f32x4_t sacc[RG][kTau4];
     if constexpr (!FP8) {
-      // Latent chunk 4ks+lg of token 16tau+ln16 sits in slot (4ks+lg) ^ ln16,
-      // i.e. at key_base ^ ((ks & 3) << 6) plus (ks >> 2) * 256 within the row.
-      const int key_base = ln16 * 1024 + ((lg ^ (ln16 & 3)) << 4) + ((ln16 >> 2) << 6);
+      // Latent chunk 4ks+lg of token 16tau+ln16 sits in slot
+      // (4ks+lg) ^ bf16_key(ln16) = 4ks ^ (lg ^ bf16_key(ln16)).
+      const int key_base = ln16 * 1024 + ((lg ^ bf16_key(ln16)) << 4);
       const int rope_base = St::kCkv + ln16 * 128;
       auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
         if (step < 2) {
@@ -481,7 +501,7 @@ void partial_kernel(const PartialParams p) {
           const int ks = step - 2;
 #pragma unroll
           for (int tau = 0; tau < kTau4; ++tau)
-            a[tau] = lds_b128(cb + tau * 16384 + (ks >> 2) * 256 + (key_base ^ ((ks & 3) << 6)));
+            a[tau] = lds_b128(cb + tau * 16384 + (key_base ^ (ks << 6)));
         }
       };
       bf16x8_t ka[3][kTau4];
@@ -626,14 +646,13 @@ void partial_kernel(const PartialParams p) {
     if constexpr (!FP8) {
       // Transposing 16-bit reads of 4 tokens x 4 columns per lane group of 4:
       // lane (x = lane >> 2, q4 = lane & 3) supplies token 32ps + 16hh + x,
-      // columns 16dt + 4q4 .. +3 = chunk 2dt + (q4 >> 1); that chunk's slot
-      // (2dt + (q4>>1)) ^ x splits into a per-lane part and (dt & 7) << 1
-      // XORed into bits 1..3, plus the 16-chunk group dt >> 3.
+      // columns 16dt + 4q4 .. +3 = half (q4 & 1) of chunk 2dt + (q4 >> 1),
+      // which sits in slot (2dt + (q4 >> 1)) ^ bf16_key(x)
+      // = 2dt ^ ((q4 >> 1) ^ bf16_key(x)).
       const int x = lv >> 2, q4 = lv & 3;
-      const int tr_base =
-          x * 1024 + ((2 * (x >> 1) + ((q4 >> 1) ^ (x & 1))) << 4) + ((q4 & 1) << 3);
+      const int tr_base = x * 1024 + (((q4 >> 1) ^ bf16_key(x)) << 4) + ((q4 & 1) << 3);
       auto tr_off = [&](int ps, int hh, int dt) {
-        return (tr_base ^ ((dt & 7) << 5)) + (dt >> 3) * 256 + ps * 32768 + hh * 16384;
+        return ps * 32768 + hh * 16384 + (tr_base ^ (dt << 5));
       };
       auto v_frag = [&](int f) {
         const int ps = f >> 5, dt = f & 31;
@@ -685,28 +704,53 @@ void partial_kernel(const PartialParams p) {
     }
   }
 
-  // ---- epilogue
+  // ---- epilogue: normalise and write each row (out = O / l, lse = m + ln l).
+  // The accumulator layout gives a lane 16 bytes of a row per column tile, so
+  // each row group is first transposed through LDS (a 32 KiB area per wave,
+  // 16-byte chunk c of row rr in slot c ^ rr) and then stored one contiguous
+  // 1 KiB half row per instruction.
   const bool direct = p.n_splits == 1;
   const int64_t part = (int64_t)r * p.n_splits + s_idx;
+  lds_barrier();  // every wave is done with the last block's LDS
+  LDS uint8_t* const stage = smem + wave * 32768;
+  const int ln = lds_opaque(lane);
 #pragma unroll
   for (int rg = 0; rg < RG; ++rg) {
     const float l_tot = xor_sum(l_run[rg]);
-    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
-    if (row >= p.rows) continue;
+    const int row0 = row_wg0 + wave * 16 * RG + rg * 16;
+    const int row = row0 + n16;
     const float lse = l_tot > 0.f ? (m_run[rg] + __log2f(l_tot)) * kLn2 : -INFINITY;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    float* dst;
-    if (direct) {
-      const int i = row / p.H, hd = row - (row / p.H) * p.H;
-      dst = p.out + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
-      if (g == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
-    } else {
-      dst = p.ws_o + (part * p.rows + row) * kDLat;
-      if (g == 0) p.ws_lse[part * p.rows + row] = lse;
+    if (g == 0 && row < p.rows) {
+      if (direct) {
+        const int i = row / p.H, hd = row - (row / p.H) * p.H;
+        p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
+      } else {
+        p.ws_lse[part * p.rows + row] = lse;
+      }
     }
-    dst += 4 * g;
 #pragma unroll
-    for (int dt = 0; dt < 32; ++dt) *(f32x4_t*)(dst + dt * 16) = scale_acc(O[dt][rg], inv);
+    for (int dt = 0; dt < 32; ++dt)
+      *(LDS f32x4_t*)(stage + n16 * 2048 + (((4 * dt + g) ^ n16) << 4)) = scale_acc(O[dt][rg], inv);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+#pragma unroll 4
+    for (int rr = 0; rr < 16; ++rr) {
+      const int rw = row0 + rr;
+      if (rw >= p.rows) break;
+      float* dst;
+      if (direct) {
+        const int i = rw / p.H, hd = rw - (rw / p.H) * p.H;
+        dst = p.out + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
+      } else {
+        dst = p.ws_o + (part * p.rows + rw) * kDLat;
+      }
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int c = 64 * half + ln;
+        *(f32x4_t*)(dst + 4 * c) = *(const LDS f32x4_t*)(stage + rr * 2048 + ((c ^ rr) << 4));
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // reads of this row group done before it is overwritten
   }
 }
 
