@@ -272,7 +272,10 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       p.ws_o = (float*)ws;
       p.ws_lse = (float*)((char*)ws + o_bytes);
     }
-    hipError_t e = mla::launch_partial(p, (int)R, fp8, row_groups, hs);
+    const int kv = !fp8 ? mla::kKvBf16
+                 : (ckv_pool->block_scale == kpe_pool->block_scale ? mla::kKvFp8Shared
+                                                                   : mla::kKvFp8Split);
+    hipError_t e = mla::launch_partial(p, (int)R, kv, row_groups, hs);
     if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
     if (S > 1) {
       mla::CombineParams c{};

@@ -67,9 +67,14 @@ struct MergeParams {
   int64_t ol_s0, ol_s1, ol_s2;
 };
 
+// Cache kinds of the partial kernel.
+constexpr int kKvBf16 = 0;
+constexpr int kKvFp8Shared = 1;  // e4m3, one scale per block for ckv and kpe
+constexpr int kKvFp8Split = 2;   // e4m3, separate ckv and kpe scales per block
+
 // Launchers; return hipSuccess or the launch error.
 // row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows)
-hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s);
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_merge(const MergeParams& p, hipStream_t s);
 

@@ -7,10 +7,12 @@
 // HBM once per workgroup and staged in LDS for all of its rows:
 //
 //   gather   direct-to-LDS 16-byte loads (global_load_lds_dwordx4) of each
-//            selected block (64 KiB latent + 8 KiB RoPE rows) into one of two
-//            LDS buffers; block i+1 streams in while block i is computed.  The
-//            chunk's block table maps the selected logical block to its pool
-//            block; one workgroup barrier per block.
+//            selected block into LDS, one block (bf16) or two (fp8) ahead of
+//            the block being computed.  The chunk's block table maps the
+//            selected logical block to its pool block.  bf16 blocks (64 KiB
+//            latent + 8 KiB RoPE rows) land directly in the compute layout;
+//            fp8 blocks (e4m3 codes, 36 KiB) land as they are and the
+//            workgroup converts them into a bf16 tile, exactly, once per block.
 //   S^T      = K . Q^T per wave for its 16*RG rows: bf16 MFMA 16x16x32, K read
 //            from LDS (b128), Q held in registers for the whole kernel.
 //   softmax  online, in the exp2 domain, with wavefront reductions; the
@@ -20,16 +22,21 @@
 //            bf16 MFMA with P^T taken straight from the S^T accumulator layout
 //            (the k index of the product is a fixed permutation of the block's
 //            tokens) and V^T read with the transposing LDS read
-//            (ds_read_b64_tr_b16) from the same staged tile, since the value is
-//            the latent part of the key (Section 3.2).  O lives in the
+//            (ds_read_b64_tr_b16) from the same tile, since the value is the
+//            latent part of the key (Section 3.2).  O lives in the
 //            accumulation registers for the whole kernel.
 //   epilogue normalised output and lse = max + ln(sum) per row, either to the
 //            caller's buffers or, under split-K, to a workspace that the
 //            combine kernel reduces with the merge algebra (Section 3.3).
 //
-// LDS swizzles (token t of the block, 16-byte chunk c of its row) keep every
-// read pattern free of bank conflicts; they are described with bf16_key and
-// fp8_key below.
+// fp8 per-block scales (Section 6.3 mentions an FP8 sparse kernel; the scale
+// granularity is this library's) stay out of the bf16 tile, which holds the
+// codes exactly: the RoPE part of the scores is weighted by the RoPE / latent
+// scale ratio before the latent part is added, the scores by the latent
+// scale, and P by the latent scale before its bf16 rounding.
+//
+// LDS swizzles (token t of the block, 16-byte chunk c of its row) are
+// described with bf16_key below.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -50,38 +57,38 @@ typedef int i32x2_t __attribute__((ext_vector_type(2)));
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
 
-// Blocks stream through a ring of LDS stages of one 64-token block each: the
-// block's latent rows followed by its RoPE rows.  bf16: 73,728 B per stage,
-// two stages.  fp8 (e4m3 codes): 36,864 B per stage, four stages.
-constexpr int kRingBytes = 2 * kBlock * (kDLat + kDPe) * 2;  // 144 KiB
+// LDS layout.  bf16 caches: two stages, each one block in the compute layout
+// (64 latent rows of 1 KiB, then 64 RoPE rows of 128 B, swizzled as described
+// at bf16_key), loaded directly by the gather; block h+1 streams in while block
+// h is computed.  fp8 caches: one compute tile in the same bf16 layout, then
+// two stages holding a block's e4m3 codes as they lie in the pool (64 latent
+// rows of 512 B, then 64 RoPE rows of 64 B); at the start of a block the
+// workgroup converts its stage into the tile, and block h+2 streams in while
+// block h is computed.  After the stages: the compacted pool-block list of the
+// slot range and, for fp8, two floats per listed block (latent scale, RoPE /
+// latent scale ratio).
 template <bool FP8>
-struct Stage {
-  static constexpr int kElt = FP8 ? 1 : 2;
-  static constexpr int kRowCkv = kDLat * kElt;  // bytes per latent row
-  static constexpr int kRowKpe = kDPe * kElt;
-  static constexpr int kCkv = kBlock * kRowCkv;
-  static constexpr int kBytes = kCkv + kBlock * kRowKpe;
-  static constexpr int kNum = kRingBytes / kBytes;
-  // direct-to-LDS loads (1 KiB per wave instruction) per wave per stage
-  static constexpr int kLoads = kBytes / 1024 / 4;
+struct Layout {
+  static constexpr int kTile = kBlock * (kDLat + kDPe) * 2;  // 72 KiB
+  static constexpr int kTileCkv = kBlock * kDLat * 2;        // latent part of a tile
+  static constexpr int kStage = FP8 ? kBlock * (kDLat + kDPe) : kTile;
+  static constexpr int kStageCkv = FP8 ? kBlock * kDLat : kTileCkv;
+  static constexpr int kStageBase = FP8 ? kTile : 0;
+  static constexpr int kNum = 2;
+  static constexpr int kLead = FP8 ? 2 : 1;  // blocks streaming ahead of the computed one
+  static constexpr int kLoads = kStage / 1024 / 4;  // 1 KiB loads per wave per stage
+  static constexpr int kList = kStageBase + kNum * kStage;
+  static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
+  static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
+  static constexpr int kTotal = kWaveCnt + 16;
 };
+static_assert(Layout<true>::kTotal <= 160 * 1024 && Layout<false>::kTotal <= 160 * 1024,
+              "LDS budget");
 constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
 
 // s_waitcnt immediate (gfx9 encoding) that waits for vmcnt <= n only.
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-
-// LDS: the stage ring, the compacted pool-block list of the slot range, and
-// for fp8 caches two floats per listed block (latent scale, RoPE / latent
-// scale ratio).
-template <bool FP8>
-struct Lds {
-  static constexpr int kList = kRingBytes;
-  static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
-  static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
-  static constexpr int kTotal = kWaveCnt + 16;
-};
-static_assert(Lds<true>::kTotal <= 160 * 1024, "LDS budget");
 
 // One direct-to-LDS load per lane: 16 bytes from src to dst + 16 * lane (dst
 // must be wave-uniform; it goes through M0).  Written as asm so that the
@@ -93,6 +100,14 @@ __device__ __forceinline__ void dma16(const uint8_t* src, LDS uint8_t* dst) {
   const uint32_t d = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(src), "s"(d) : "memory", "m0");
+}
+
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset: the address needs no per-lane 64-bit arithmetic.
+__device__ __forceinline__ void dma16s(const uint8_t* base, uint32_t off, LDS uint8_t* dst) {
+  const uint32_t d = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(d) : "memory", "m0");
 }
 
 __device__ __forceinline__ bf16x8_t lds_b128(const LDS uint8_t* p) {
@@ -267,62 +282,52 @@ __device__ __forceinline__ int lds_opaque(int v) {
 // LDS traffic is not the limit.
 __device__ __forceinline__ int bf16_key(int t) { return t & 15; }
 
-// Swizzle key of token t (0..63) in an fp8 latent stage: 16-byte chunk c of
-// the token's 512-byte row sits in slot c ^ fp8_key(t).
-__device__ __forceinline__ int fp8_key(int t) { return (t & 15) ^ ((t & 16) >> 1); }
-
-// Issue direct-to-LDS loads j0 .. j1-1 (of Stage<FP8>::kLoads per wave) of
-// pool block b into a stage.
-//   bf16: load j < 16 is latent row 16w + j (1 KiB; chunk c in slot
-//         c ^ bf16_key(t)); loads 16, 17 are RoPE rows 16w .. 16w+7 and
-//         16w+8 .. 16w+15 (chunk c in slot c ^ ((t >> 1) & 7)).
-//   fp8:  load j < 8 is latent rows 16w + 2j, 16w + 2j + 1 (512 bytes each;
-//         chunk c in slot c ^ fp8_key(t)); load 8 is RoPE rows 16w .. 16w+15
-//         (64 bytes each; chunk c in slot c ^ ((t >> 2) & 3)).
+// Issue the direct-to-LDS loads of pool block b into a stage (Layout::kLoads
+// 1 KiB loads per wave).
+//   bf16: load j < 16 of wave w is latent row t = 16w + j (lane loads chunk
+//         lane ^ bf16_key(t) of the row); loads 16, 17 are RoPE rows
+//         16w .. 16w+7 and 16w+8 .. 16w+15 (chunk c in slot c ^ ((t >> 1) & 7)).
+//   fp8:  the stage is a plain copy: wave w loads latent bytes 8w .. 8w+7 KiB
+//         and RoPE bytes w .. w+1 KiB of the block.
 template <bool FP8>
-__device__ __forceinline__ void issue_part(const PartialParams& p, int64_t b, LDS uint8_t* buf,
-                                           int wave, int lane_in, int j0, int j1) {
-  using St = Stage<FP8>;
+__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, LDS uint8_t* buf,
+                                            int wave, int lane_in) {
+  using Ly = Layout<FP8>;
   // Recompute the per-lane source offsets at every issue instead of letting
   // them be hoisted out of the main loop: registers are scarce there.
   int lane;
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
-  const uint8_t* ckv = p.ckv + b * St::kCkv;
-  const uint8_t* kpe = p.kpe + b * (kBlock * St::kRowKpe);
+  const uint32_t lane16 = (uint32_t)lane << 4;
+  const uint8_t* ckv = p.ckv + b * Ly::kStageCkv;
+  const uint8_t* kpe = p.kpe + b * (Ly::kStage - Ly::kStageCkv);
+  if constexpr (!FP8) {
 #pragma unroll
-  for (int j = j0; j < j1; ++j) {
-    if constexpr (!FP8) {
-      if (j < 16) {
-        const int t = wave * 16 + j;
-        dma16(ckv + t * St::kRowCkv + ((lane ^ bf16_key(t)) << 4), buf + t * 1024);
-      } else {
-        const int k = wave * 2 + (j - 16);  // 1 KiB = RoPE rows 8k .. 8k+7
-        const int t = 8 * k + (lane >> 3);
-        const int c = (lane & 7) ^ ((t >> 1) & 7);
-        dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + k * 1024);
-      }
-    } else {
-      if (j < 8) {
-        const int k = wave * 8 + j;  // 1 KiB = latent rows 2k, 2k+1
-        const int t = 2 * k + (lane >> 5);
-        const int c = (lane & 31) ^ fp8_key(t);
-        dma16(ckv + t * St::kRowCkv + (c << 4), buf + k * 1024);
-      } else {
-        const int t = wave * 16 + (lane >> 2);  // 1 KiB = RoPE rows 16w .. 16w+15
-        const int c = (lane & 3) ^ ((t >> 2) & 3);
-        dma16(kpe + t * St::kRowKpe + (c << 4), buf + St::kCkv + wave * 1024);
-      }
+    for (int j = 0; j < 16; ++j) {
+      const int t = wave * 16 + j;
+      dma16s(ckv + t * 1024, lane16 ^ (uint32_t)(bf16_key(t) << 4), buf + t * 1024);
     }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
+      const int t = 8 * k + (lane >> 3);
+      const int c = (lane & 7) ^ ((t >> 1) & 7);
+      dma16(kpe + t * 128 + (c << 4), buf + Ly::kStageCkv + k * 1024);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = wave * 8 + j;
+      dma16s(ckv + k * 1024, lane16, buf + k * 1024);
+    }
+    dma16s(kpe + wave * 1024, lane16, buf + Ly::kStageCkv + wave * 1024);
   }
 }
 
 // Wait until at most `stages` later stages of this wave's loads are in flight.
 template <bool FP8>
 __device__ __forceinline__ void wait_stages(int stages) {
-  constexpr int L = Stage<FP8>::kLoads;
-  if (stages >= 2)
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * L));
-  else if (stages == 1)
+  constexpr int L = Layout<FP8>::kLoads;
+  if (stages >= 1)
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(L));
   else
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
@@ -341,19 +346,77 @@ __device__ __forceinline__ bf16x8_t e4m3x8_bf16(uint32_t w0, uint32_t w1) {
                                               e4m3x2_bf16<false>(w1), e4m3x2_bf16<true>(w1)});
 }
 
+// Convert a stage of e4m3 codes into the bf16 compute tile: 4608 units of 8
+// codes (64 latent rows x 64 units, then 64 RoPE rows x 8 units), 18 per lane.
+// In each round a wave converts 64 consecutive units: it reads 512 contiguous
+// bytes and writes one latent row (or 8 RoPE rows) of the tile.  The codes
+// are converted exactly (every e4m3 value is a bf16 value); the block scales
+// are applied to the products in fp32.
+__device__ __forceinline__ void convert_stage(const LDS uint8_t* st, LDS uint8_t* tile, int tid) {
+  constexpr int kCkvUnits = kBlock * kDLat / 8;
+  constexpr int kGroup = 3;  // rounds in flight (bounds the registers it takes)
+#pragma unroll
+  for (int it0 = 0; it0 < 18; it0 += kGroup) {
+    i32x2_t w[kGroup];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) w[k] = *(const LDS i32x2_t*)(st + ((it0 + k) * 256 + tid) * 8);
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int it = it0 + k, u = it * 256 + tid;
+      const bf16x8_t v = e4m3x8_bf16((uint32_t)w[k][0], (uint32_t)w[k][1]);
+      if (it < 16) {
+        const int t = u >> 6, c = u & 63;
+        *(LDS bf16x8_t*)(tile + t * 1024 + ((c ^ bf16_key(t)) << 4)) = v;
+      } else {
+        const int ur = u - kCkvUnits, t = ur >> 3, c = ur & 7;
+        *(LDS bf16x8_t*)(tile + kBlock * 1024 + t * 128 + ((c ^ ((t >> 1) & 7)) << 4)) = v;
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Value fragments of O^T += V^T . P^T from a bf16 tile: fragment f = 32ps + dt
+// (k-step ps, column tile dt) must list, for lane (g = lane >> 4, c = lane &
+// 15), column 16dt + c of the tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}, in that
+// order (the token order of P^T as the S^T products leave it).  Transposing
+// 16-bit reads of 4 tokens x 4 columns per lane group of 4: lane (x = lane >> 2,
+// q4 = lane & 3) supplies token 32ps + 16hh + x, columns 16dt + 4q4 .. +3 =
+// half (q4 & 1) of chunk 2dt + (q4 >> 1), which sits in slot
+// (2dt + (q4 >> 1)) ^ bf16_key(x) = 2dt ^ ((q4 >> 1) ^ bf16_key(x)).
+struct VFrags {
+  const LDS uint8_t* cb;
+  int tr_base;
+  __device__ __forceinline__ VFrags(const LDS uint8_t* cb_, int lv) : cb(cb_) {
+    const int x = lv >> 2, q4 = lv & 3;
+    tr_base = x * 1024 + (((q4 >> 1) ^ bf16_key(x)) << 4) + ((q4 & 1) << 3);
+  }
+  __device__ __forceinline__ bf16x8_t load(int f) const {
+    const int ps = f >> 5, dt = f & 31;
+    const int o = ps * 32768 + (tr_base ^ (dt << 5));
+    const i16x4_t lo = lds_tr16(cb + o);
+    const i16x4_t hi = lds_tr16(cb + o + 16384);
+    return __builtin_bit_cast(bf16x8_t,
+                              i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+  }
+};
+
 // RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
-// of the row tile (64*RG rows) over all 512 latent columns.  FP8 selects e4m3
-// cache pools with per-block scales.
-template <int RG, bool FP8>
+// of the row tile (64*RG rows) over all 512 latent columns.  KV is the cache
+// kind: bf16, e4m3 with one scale per block for the whole 576-wide entries, or
+// e4m3 with separate latent and RoPE scales per block.
+template <int RG, int KV>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void partial_kernel(const PartialParams p) {
-  using St = Stage<FP8>;
-  using L = Lds<FP8>;
+  constexpr bool FP8 = KV != kKvBf16;
+  constexpr bool kSplitScales = KV == kKvFp8Split;
+  using L = Layout<FP8>;
   constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
   constexpr int kKSteps = kBlock / 32;  // 32-token PV k-steps per block
   constexpr int kRowsWg = 64 * RG;
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
   LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
+  LDS uint8_t* const stage0 = smem + L::kStageBase;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -407,10 +470,10 @@ void partial_kernel(const PartialParams p) {
     lds_barrier();
   }
 
-  // ---- the first stages' loads go out before the query rows, so that their
+  // ---- the first blocks' loads go out before the query rows, so that their
   // latencies overlap
-  for (int h = 0; h < n_valid && h < St::kNum - 1; ++h)
-    issue_part<FP8>(p, list[h], smem + h * St::kBytes, wave, lane, 0, St::kLoads);
+  for (int h = 0; h < n_valid && h < L::kLead; ++h)
+    issue_stage<FP8>(p, list[h], stage0 + h * L::kStage, wave, lane);
 
   // ---- this wave's query rows as MFMA B operands, held for the whole kernel:
   // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
@@ -450,32 +513,40 @@ void partial_kernel(const PartialParams p) {
     l_run[rg] = 0.f;
   }
 
-  // ---- main loop over the listed blocks: up to St::kNum - 1 blocks stream in
-  // while one is computed
+  // ---- main loop over the listed blocks; L::kLead blocks stream in while one
+  // is computed
   for (int h = 0; h < n_valid; ++h) {
-    wait_stages<FP8>(min(n_valid - 1 - h, St::kNum - 2));
+    wait_stages<FP8>(min(n_valid - 1 - h, L::kLead - 1));
     lds_barrier();  // block h is in LDS for every wave; every wave is done with block h-1
-    {
-      // All of the next stage's loads at once: spreading them between the
-      // products measured slower (each load holds the issuing wave until the
-      // shared address unit takes it, and the stage's LDS reads then compete
-      // with the incoming writes).
-      const int hn = h + St::kNum - 1;
-      if (hn < n_valid)
-        issue_part<FP8>(p, list[hn], smem + (hn % St::kNum) * St::kBytes, wave, lane, 0,
-                        St::kLoads);
-    }
-    const LDS uint8_t* cb = smem + (h % St::kNum) * St::kBytes;
-    // fp8: the block's latent scale and RoPE / latent scale ratio.  The scores
-    // are accumulated as ratio * (q_pe . kpe codes) + q_lat . ckv codes and then
-    // scaled by scale * latent scale; P is scaled by the latent scale for PV.
+    // The pool block that streams into the stage freed by this block (read
+    // from LDS first: LDS reads complete in order).
+    const int hn = h + L::kLead;
+    const int b_next = hn < n_valid ? __builtin_amdgcn_readfirstlane(list[hn]) : -1;
+    __builtin_amdgcn_sched_barrier(0);
+    // fp8: the scores are accumulated as ratio * (q_pe . kpe codes) +
+    // q_lat . ckv codes (ratio = RoPE scale / latent scale) and then scaled by
+    // the softmax scale times the latent scale; P is scaled by the latent
+    // scale before its bf16 rounding.
     float s_mult = p.scale_log2, v_mult = 1.f, pe_ratio = 1.f;
+    const LDS uint8_t* cb;
     if constexpr (FP8) {
       v_mult = scales[2 * h];
-      pe_ratio = scales[2 * h + 1];
+      if constexpr (kSplitScales) pe_ratio = scales[2 * h + 1];
       s_mult = p.scale_log2 * v_mult;
+      convert_stage(stage0 + (h % L::kNum) * L::kStage, smem, tid);
+      lds_barrier();  // the tile is complete; every wave is done with the stage
+      cb = smem;
+    } else {
+      cb = stage0 + (h % L::kNum) * L::kStage;
     }
-
+    // The next stage's loads, all at once, right after the first key reads of
+    // this block (whose latency they cover).  Spreading them between the
+    // products measured slower: the per-CU address unit takes about one 1 KiB
+    // load per 18 cycles and holds each issuing wave until it does.
+    auto issue_next = [&]() {
+      if (b_next >= 0) issue_stage<FP8>(p, b_next, stage0 + (hn % L::kNum) * L::kStage, wave, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    };
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
     // every iteration (a few VALU ops) rather than held in registers across
     // the loop.
@@ -487,11 +558,11 @@ void partial_kernel(const PartialParams p) {
     // requested about two steps before their products; the scheduling fences
     // keep the compiler from regrouping loads next to their use.
     f32x4_t sacc[RG][kTau4];
-    if constexpr (!FP8) {
+    {
       // Latent chunk 4ks+lg of token 16tau+ln16 sits in slot
       // (4ks+lg) ^ bf16_key(ln16) = 4ks ^ (lg ^ bf16_key(ln16)).
       const int key_base = ln16 * 1024 + ((lg ^ bf16_key(ln16)) << 4);
-      const int rope_base = St::kCkv + ln16 * 128;
+      const int rope_base = L::kTileCkv + ln16 * 128;
       auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
         if (step < 2) {
 #pragma unroll
@@ -507,6 +578,7 @@ void partial_kernel(const PartialParams p) {
       bf16x8_t ka[3][kTau4];
       key_frags(0, ka[0]);
       key_frags(1, ka[1]);
+      issue_next();
 #pragma unroll
       for (int step = 0; step < 18; ++step) {
         if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
@@ -515,72 +587,35 @@ void partial_kernel(const PartialParams p) {
         bf16x8_t q[RG];
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
-        if (step == 0)
-          StGroup<RG, kTau4, true, false, false>::run(sacc, ka[0], q);
-        else if (step == 17)
-          StGroup<RG, kTau4, false, true, false>::run(sacc, ka[step % 3], q);
-        else
-          StGroup<RG, kTau4, false, false, false>::run(sacc, ka[step % 3], q);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-      // One 8-byte read per lane and tile per k-step: latent dims 32ks + 8lg
-      // of token t = 16tau + ln16 are half (lg & 1) of chunk 2ks + (lg >> 1),
-      // which sits in slot (2ks + (lg >> 1)) ^ fp8_key(t), fp8_key(t) =
-      // ln16 ^ 8(tau & 1); RoPE dims 32ks + 8lg are half (lg & 1) of chunk
-      // 2ks + (lg >> 1) of the token's 64-byte RoPE row, in slot
-      // chunk ^ ((t >> 2) & 3).
-      const int key_base =
-          ln16 * St::kRowCkv + ((((lg >> 1) ^ ln16)) << 4) + ((lg & 1) << 3);
-      const int rope_base = St::kCkv + ln16 * St::kRowKpe + ((lg & 1) << 3);
-      const int rope_key = (ln16 >> 2) & 3;
-      auto key_raw = [&](int step, i32x2_t (&a)[kTau4]) {
-        if (step < 2) {
-#pragma unroll
-          for (int tau = 0; tau < kTau4; ++tau)
-            a[tau] = *(const LDS i32x2_t*)(cb + rope_base + tau * 16 * St::kRowKpe +
-                                          (((2 * step + (lg >> 1)) ^ rope_key) << 4));
-        } else {
-          const int ks = step - 2;
-#pragma unroll
-          for (int tau = 0; tau < kTau4; ++tau)
-            a[tau] = *(const LDS i32x2_t*)(cb + tau * 16 * St::kRowCkv +
-                                          (key_base ^ (ks << 5) ^ ((tau & 1) << 7)));
-        }
-      };
-      i32x2_t kr[3][kTau4];
-      key_raw(0, kr[0]);
-      key_raw(1, kr[1]);
-#pragma unroll
-      for (int step = 0; step < 18; ++step) {
-        if (step + 2 < 18) key_raw(step + 2, kr[(step + 2) % 3]);
-        __builtin_amdgcn_sched_barrier(0);
-        const int ks = step < 2 ? 16 + step : step - 2;
-        bf16x8_t a[kTau4], q[RG];
-#pragma unroll
-        for (int tau = 0; tau < kTau4; ++tau)
-          a[tau] = e4m3x8_bf16((uint32_t)kr[step % 3][tau][0], (uint32_t)kr[step % 3][tau][1]);
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
         if (step == 0) {
-          StGroup<RG, kTau4, true, false, true>::run(sacc, a, q);
-        } else if (step == 1 || step == 17) {
-          StGroup<RG, kTau4, false, true, true>::run(sacc, a, q);
+          StGroup<RG, kTau4, true, false, false>::run(sacc, ka[0], q);
+        } else if (step == 17 || (kSplitScales && step == 1)) {
+          StGroup<RG, kTau4, false, true, false>::run(sacc, ka[step % 3], q);
+        } else if (kSplitScales && step == 2) {
+          // The RoPE part is complete: weight it by the scale ratio, in place;
+          // the group's lead covers this VALU write of its accumulators.
+#pragma unroll
+          for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
+          StGroup<RG, kTau4, false, false, true>::run(sacc, ka[step % 3], q);
         } else {
-          if (step == 2) {
-            // The RoPE part is complete: weight it by its scale relative to
-            // the latent scale, in place (the next group's lead covers this
-            // VALU write of its accumulators).
-#pragma unroll
-            for (int rg = 0; rg < RG; ++rg)
-#pragma unroll
-              for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
-          }
-          StGroup<RG, kTau4, false, false, true>::run(sacc, a, q);
+          StGroup<RG, kTau4, false, false, false>::run(sacc, ka[step % 3], q);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+
+    // The first value fragments of O^T += V^T . P^T are requested before the
+    // softmax, whose VALU work then covers their latency.
+    constexpr int kPvAhead = 8;
+    constexpr int kFrags = 32 * kKSteps;
+    const VFrags vf(cb, lds_opaque(lane));
+    bf16x8_t vr[kPvAhead + 1];
+#pragma unroll
+    for (int f = 0; f < kPvAhead; ++f) vr[f] = vf.load(f);
+    __builtin_amdgcn_sched_barrier(0);
+
     f32x4_t acc[RG][kTau4];
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg)
@@ -618,90 +653,52 @@ void partial_kernel(const PartialParams p) {
         }
       }
     }
-    // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}.
-    // The row sum takes the unrounded fp32 weights; the PV operand is rounded
-    // to bf16 (after the latent scale, for fp8).
+    // P^T B operands: k-step ps covers tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}
+    // (token tiles 2ps and 2ps+1).  The row sum takes the unrounded fp32
+    // weights; the PV operand is rounded to bf16 (after the latent scale, for
+    // fp8).  The weights of k-step 0 are computed here; those of k-step 1 are
+    // computed two at a time between the products of k-step 0, which does not
+    // need them, so that this VALU work runs beside the matrix core.
     bf16x8_t pb[RG][kKSteps];
+    float psum[RG];
+    auto p_pair = [&](int rg, int tau, int k0) {
+      const float e0 = __builtin_amdgcn_exp2f(acc[rg][tau][k0] - m_run[rg]);
+      const float e1 = __builtin_amdgcn_exp2f(acc[rg][tau][k0 + 1] - m_run[rg]);
+      psum[rg] += e0 + e1;
+      pb[rg][tau >> 1][(tau & 1) * 4 + k0] = (__bf16)(FP8 ? e0 * v_mult : e0);
+      pb[rg][tau >> 1][(tau & 1) * 4 + k0 + 1] = (__bf16)(FP8 ? e1 * v_mult : e1);
+    };
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
-      float ps = 0.f;
+      psum[rg] = 0.f;
 #pragma unroll
-      for (int tau = 0; tau < kTau4; ++tau)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float e = __builtin_amdgcn_exp2f(acc[rg][tau][k] - m_run[rg]);
-          ps += e;
-          pb[rg][tau >> 1][(tau & 1) * 4 + k] = (__bf16)(FP8 ? e * v_mult : e);
-        }
-      l_run[rg] += ps;
+      for (int tau = 0; tau < 2; ++tau) {
+        p_pair(rg, tau, 0);
+        p_pair(rg, tau, 2);
+      }
     }
+    // pair i (i < 4 * RG) of k-step 1: row group i >> 2, tile 2 + ((i >> 1) & 1),
+    // elements 2 (i & 1) and 2 (i & 1) + 1
+    constexpr int kLatePairs = 4 * RG;
+    constexpr int kLateStride = 32 / kLatePairs;
 
     // O^T[dim][row] += V^T . P^T over 2 k-steps x 32 column tiles, in a
-    // software pipeline kPvAhead fragments deep.  The value fragment of k-step
-    // ps and column tile dt must list, for lane (g, c), column 16dt + c of the
-    // tokens 32ps + {4g..4g+3, 16+4g..16+4g+3}, in that order.
-    constexpr int kPvAhead = 8;
-    constexpr int kFrags = 32 * kKSteps;
-    const int lv = lds_opaque(lane);
-    if constexpr (!FP8) {
-      // Transposing 16-bit reads of 4 tokens x 4 columns per lane group of 4:
-      // lane (x = lane >> 2, q4 = lane & 3) supplies token 32ps + 16hh + x,
-      // columns 16dt + 4q4 .. +3 = half (q4 & 1) of chunk 2dt + (q4 >> 1),
-      // which sits in slot (2dt + (q4 >> 1)) ^ bf16_key(x)
-      // = 2dt ^ ((q4 >> 1) ^ bf16_key(x)).
-      const int x = lv >> 2, q4 = lv & 3;
-      const int tr_base = x * 1024 + (((q4 >> 1) ^ bf16_key(x)) << 4) + ((q4 & 1) << 3);
-      auto tr_off = [&](int ps, int hh, int dt) {
-        return ps * 32768 + hh * 16384 + (tr_base ^ (dt << 5));
-      };
-      auto v_frag = [&](int f) {
-        const int ps = f >> 5, dt = f & 31;
-        const i16x4_t lo = lds_tr16(cb + tr_off(ps, 0, dt));
-        const i16x4_t hi = lds_tr16(cb + tr_off(ps, 1, dt));
-        return __builtin_bit_cast(bf16x8_t,
-                                  i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-      };
-      bf16x8_t va[kPvAhead + 1];
+    // software pipeline kPvAhead fragments deep.
 #pragma unroll
-      for (int f = 0; f < kPvAhead; ++f) va[f] = v_frag(f);
-#pragma unroll
-      for (int f = 0; f < kFrags; ++f) {
-        if (f + kPvAhead < kFrags) va[(f + kPvAhead) % (kPvAhead + 1)] = v_frag(f + kPvAhead);
-        __builtin_amdgcn_sched_barrier(0);
-        const int ps = f >> 5, dt = f & 31;
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-          O[dt][rg] = mfma(va[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
-        __builtin_amdgcn_sched_barrier(0);
+    for (int f = 0; f < kFrags; ++f) {
+      if (f + kPvAhead < kFrags) vr[(f + kPvAhead) % (kPvAhead + 1)] = vf.load(f + kPvAhead);
+      if (f < 32 && f % kLateStride == 0) {
+        const int i = f / kLateStride;
+        p_pair(i >> 2, 2 + ((i >> 1) & 1), 2 * (i & 1));
       }
-    } else {
-      // One transposing 8-bit read per fragment: in each 16-lane group, lane
-      // 2j + q supplies 8 columns (16dt + 8q ..) of the fragment's j-th token
-      // and lane c receives column 16dt + c of the 8 tokens.  Token
-      // 32ps + 16(j >> 2) + 4g + (j & 3) has swizzle key 4g + (j & 3) ^ 8(j >> 2).
-      const int c = lv & 15, j = c >> 1, gq = lv >> 4;
-      const int key = (4 * gq + (j & 3)) ^ ((j >> 2) << 3);
-      const int tr_base = (16 * (j >> 2) + 4 * gq + (j & 3)) * St::kRowCkv + (key << 4) + ((c & 1) << 3);
-      auto v_raw = [&](int f) {
-        const int ps = f >> 5, dt = f & 31;
-        return __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-            (LDS i32x2_t*)(cb + ps * 32 * St::kRowCkv + (tr_base ^ (dt << 4))));
-      };
-      i32x2_t vr[kPvAhead + 1];
+      __builtin_amdgcn_sched_barrier(0);
+      const int ps = f >> 5, dt = f & 31;
 #pragma unroll
-      for (int f = 0; f < kPvAhead; ++f) vr[f] = v_raw(f);
-#pragma unroll
-      for (int f = 0; f < kFrags; ++f) {
-        if (f + kPvAhead < kFrags) vr[(f + kPvAhead) % (kPvAhead + 1)] = v_raw(f + kPvAhead);
-        __builtin_amdgcn_sched_barrier(0);
-        const int ps = f >> 5, dt = f & 31;
-        const i32x2_t w = vr[f % (kPvAhead + 1)];
-        const bf16x8_t va = e4m3x8_bf16((uint32_t)w[0], (uint32_t)w[1]);
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(va, pb[rg][ps], O[dt][rg]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(vr[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg) l_run[rg] += psum[rg];
   }
 
   // ---- epilogue: normalise and write each row (out = O / l, lse = m + ln l).
@@ -756,20 +753,23 @@ void partial_kernel(const PartialParams p) {
 
 }  // namespace
 
-hipError_t launch_partial(const PartialParams& p, int R, bool fp8, int row_groups, hipStream_t s) {
+template <int KV>
+static void launch_kv(const PartialParams& p, int grid, int row_groups, hipStream_t s) {
+  if (row_groups == 2)
+    hipLaunchKernelGGL((partial_kernel<2, KV>), dim3(grid), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((partial_kernel<1, KV>), dim3(grid), dim3(256), 0, s, p);
+}
+
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, hipStream_t s) {
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (fp8) {
-    if (row_groups == 2)
-      hipLaunchKernelGGL((partial_kernel<2, true>), dim3(grid), dim3(256), 0, s, p);
-    else
-      hipLaunchKernelGGL((partial_kernel<1, true>), dim3(grid), dim3(256), 0, s, p);
-  } else {
-    if (row_groups == 2)
-      hipLaunchKernelGGL((partial_kernel<2, false>), dim3(grid), dim3(256), 0, s, p);
-    else
-      hipLaunchKernelGGL((partial_kernel<1, false>), dim3(grid), dim3(256), 0, s, p);
-  }
+  if (kv == kKvFp8Shared)
+    launch_kv<kKvFp8Shared>(p, grid, row_groups, s);
+  else if (kv == kKvFp8Split)
+    launch_kv<kKvFp8Split>(p, grid, row_groups, s);
+  else
+    launch_kv<kKvBf16>(p, grid, row_groups, s);
   return hipGetLastError();
 }
 

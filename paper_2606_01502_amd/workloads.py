@@ -17,9 +17,10 @@ tensor is the same whatever the thread count):
   * a job's selection is drawn without replacement and sorted ascending;
   * the pool is scattered: logical block -> pool block goes through a
     seeded permutation of the pool;
-  * fp8 caches are the same values quantised per 64-token block and per
-    tensor (ckv, kpe separately) to OCP E4M3FN with scale absmax / 448,
-    round-to-nearest-even, saturating at +-448 (absmax 0 gives scale 1).
+  * fp8 caches are the same values quantised per 64-token block to OCP
+    E4M3FN with scale absmax / 448 over the block's 576-wide entries (one
+    scale for ckv and kpe; separate scales on request), round-to-nearest-even,
+    saturating at +-448 (absmax 0 gives scale 1).
 """
 from __future__ import annotations
 
@@ -111,30 +112,31 @@ def quantize_e4m3fn(y: np.ndarray) -> np.ndarray:
     return code.astype(np.uint8) | sign
 
 
-def quantize_blocks_e4m3fn(bits: np.ndarray):
-    """Per-block fp8 quantisation of a bf16 pool [P, 64, D].
+def quantize_blocks_e4m3fn(*pools: np.ndarray):
+    """Per-block fp8 quantisation of bf16 pools [P, 64, D_i] that share one
+    scale per block: scale = float32(absmax / 448) over the block's values in
+    all the given pools (1 when that absmax is 0), code = E4M3FN(value / scale).
 
-    Returns (codes uint8 [P, 64, D], scales float32 [P]) with
-    scale = float32(absmax / 448) (1 when absmax is 0) and
-    code = E4M3FN(value / scale).
+    Returns (codes uint8 per pool..., scales float32 [P]).
     """
-    P = bits.shape[0]
-    codes = np.empty(bits.shape, np.uint8)
+    P = pools[0].shape[0]
+    codes = [np.empty(b.shape, np.uint8) for b in pools]
     scales = np.empty(P, np.float32)
     step = 16  # small chunks: temporaries of a few MB are reused from the heap
 
     def work(lo):
         hi = min(P, lo + step)
-        x = bf16_bits_to_f32(bits[lo:hi])
-        amax = np.abs(x).reshape(hi - lo, -1).max(axis=1)
+        xs = [bf16_bits_to_f32(b[lo:hi]) for b in pools]
+        amax = np.max([np.abs(x).reshape(hi - lo, -1).max(axis=1) for x in xs], axis=0)
         s = (amax / np.float32(E4M3_MAX)).astype(np.float32)
         s[amax == 0] = np.float32(1.0)
         scales[lo:hi] = s
-        codes[lo:hi] = quantize_e4m3fn(x.astype(np.float64) / s.astype(np.float64)[:, None, None])
+        for c, x in zip(codes, xs):
+            c[lo:hi] = quantize_e4m3fn(x.astype(np.float64) / s.astype(np.float64)[:, None, None])
 
     with ThreadPoolExecutor(_threads()) as ex:
         list(ex.map(work, range(0, P, step)))
-    return codes, scales
+    return (*codes, scales)
 
 
 # ------------------------------------------------------------------ workloads
@@ -180,10 +182,17 @@ class Workload:
             b += self.n_selected_blocks() * 8  # two fp32 scales per block
         return b
 
-    def to_fp8(self):
-        """The same values with E4M3FN caches (per-block absmax/448 scales)."""
-        ckv, cs = quantize_blocks_e4m3fn(self.ckv)
-        kpe, ks = quantize_blocks_e4m3fn(self.kpe)
+    def to_fp8(self, shared_scale=True):
+        """The same values with E4M3FN caches and per-block absmax/448 scales:
+        one scale per block for the whole 576-wide entries (the same array for
+        ckv_scale and kpe_scale), or with shared_scale=False separate latent
+        and RoPE scales."""
+        if shared_scale:
+            ckv, kpe, cs = quantize_blocks_e4m3fn(self.ckv, self.kpe)
+            ks = cs
+        else:
+            ckv, cs = quantize_blocks_e4m3fn(self.ckv)
+            kpe, ks = quantize_blocks_e4m3fn(self.kpe)
         return Workload(self.name + "-fp8", self.q_lat, self.q_pe, ckv, kpe, self.table,
                         self.sel, self.scale, cs, ks, self.n_requests, self.merge_parts,
                         dict(self.meta))

@@ -32,7 +32,9 @@ def upload(w):
         t["ckv"] = torch.from_numpy(np.ascontiguousarray(w.ckv)).to(dev)
         t["kpe"] = torch.from_numpy(np.ascontiguousarray(w.kpe)).to(dev)
         t["ckv_scale"] = torch.from_numpy(np.ascontiguousarray(w.ckv_scale)).to(dev)
-        t["kpe_scale"] = torch.from_numpy(np.ascontiguousarray(w.kpe_scale)).to(dev)
+        # one array for both pools selects the library's shared-scale path
+        t["kpe_scale"] = (t["ckv_scale"] if w.kpe_scale is w.ckv_scale else
+                          torch.from_numpy(np.ascontiguousarray(w.kpe_scale)).to(dev))
     else:
         t["ckv"] = bf16(w.ckv)
         t["kpe"] = bf16(w.kpe)

@@ -1,9 +1,11 @@
 """fp8-e4m3 latent-cache path against the oracle on the dequantised values.
 
-The cache pools hold OCP E4M3FN codes with one fp32 scale per 64-token block
-and pool (ckv and kpe separately).  The oracle decodes every code exactly
-and multiplies by the block scale in fp64; the GPU path must meet the same
-bar as bf16 (row-normwise 1e-2, lse 1e-3).
+The cache pools hold OCP E4M3FN codes with fp32 scales per 64-token block:
+one scale for the whole 576-wide entries (the same array passed for both
+pools), or separate latent and RoPE scales (two arrays), which the library
+handles on a path of its own.  The oracle decodes every code exactly and
+multiplies by the block scale in fp64; the GPU path must meet the same bar as
+bf16 (row-normwise 1e-2, lse 1e-3).
 """
 import numpy as np
 import pytest
@@ -29,25 +31,27 @@ def _check(w, n_splits=0, what="", jobs=None):
     return G.assert_parity(out, lse, ref_o, ref_l, what or w.name)
 
 
+@pytest.mark.parametrize("shared", [True, False])
 @pytest.mark.parametrize("n_splits", [0, 1, 3, 7])
-def test_fp8_random_splits(n_splits):
-    print(f"case: fp8 random splits={n_splits}", flush=True)
-    w = W.random_case(201, R=3, Mq=1, H=128, P=20, NB=9, K=7, sigma=0.5).to_fp8()
+def test_fp8_random_splits(n_splits, shared):
+    print(f"case: fp8 random splits={n_splits} shared={shared}", flush=True)
+    w = W.random_case(201, R=3, Mq=1, H=128, P=20, NB=9, K=7, sigma=0.5).to_fp8(shared)
     _check(w, n_splits)
 
 
 @pytest.mark.parametrize("mq,h", [(1, 1), (1, 16), (2, 40), (1, 64), (3, 64), (2, 128), (5, 31)])
 def test_fp8_ragged_rows(mq, h):
     print(f"case: fp8 ragged mq={mq} h={h}", flush=True)
-    w = W.random_case(202 + 1000 * mq + h, R=2, Mq=mq, H=h, P=12, NB=6, K=3,
-                      sigma=0.7).to_fp8()
-    _check(w)
+    w = W.random_case(202 + 1000 * mq + h, R=2, Mq=mq, H=h, P=12, NB=6, K=3, sigma=0.7)
+    _check(w.to_fp8(), 0, f"ragged {mq}x{h} shared")
+    _check(w.to_fp8(shared_scale=False), 0, f"ragged {mq}x{h} separate")
 
 
-def test_fp8_padding_duplicates_empty():
-    print("case: fp8 padding", flush=True)
+@pytest.mark.parametrize("shared", [True, False])
+def test_fp8_padding_duplicates_empty(shared):
+    print(f"case: fp8 padding shared={shared}", flush=True)
     w = W.random_case(203, R=4, Mq=1, H=32, P=10, NB=6, K=6, n_valid=[0, 1, 3, 6],
-                      allow_dup=True, pad_pattern="interleaved").to_fp8()
+                      allow_dup=True, pad_pattern="interleaved").to_fp8(shared)
     for s in (0, 1, 2, 6):
         _check(w, s, f"fp8 padding splits={s}")
 
@@ -68,18 +72,22 @@ def _every_code_pool(seed, P):
     return ckv, kpe
 
 
-@pytest.mark.parametrize("ratio", [1.0, 37.0, 1.0 / 53.0])
+@pytest.mark.parametrize("ratio", [None, 1.0, 37.0, 1.0 / 53.0])
 def test_fp8_every_code_and_scale_ratios(ratio):
     """All 254 finite codes, including +-448, the subnormals and -0, under
-    per-block scales that differ from block to block and between the latent
-    and RoPE pools by `ratio`."""
+    per-block scales that differ from block to block; ratio None passes one
+    scale array for both pools, otherwise the RoPE scales differ from the
+    latent ones by about `ratio`."""
     print(f"case: fp8 every code ratio={ratio}", flush=True)
     P = 10
     base = W.random_case(204, R=2, Mq=1, H=128, P=P, NB=8, K=8, n_valid=[8, 5])
     ckv, kpe = _every_code_pool(204, P)
     rng = np.random.default_rng([204, 78])
     cs = (rng.uniform(0.3, 3.0, P) / 448.0).astype(np.float32)
-    ks = (cs * np.float32(ratio) * rng.uniform(0.5, 2.0, P)).astype(np.float32)
+    if ratio is None:
+        ks = cs
+    else:
+        ks = (cs * np.float32(ratio) * rng.uniform(0.5, 2.0, P)).astype(np.float32)
     w = W.Workload("every-code", base.q_lat, base.q_pe, ckv, kpe, base.table, base.sel,
                    ckv_scale=cs, kpe_scale=ks)
     for s in (0, 1, 3):
@@ -96,12 +104,14 @@ def test_fp8_zero_blocks():
     w.ckv[[1, 4]] = 0
     w.kpe[[1, 4]] = 0
     w.kpe[6] = 0  # RoPE part zero, latent part not
-    _check(w.to_fp8(), 0, "fp8 zero blocks")
+    _check(w.to_fp8(), 0, "fp8 zero blocks shared")
+    _check(w.to_fp8(shared_scale=False), 0, "fp8 zero blocks separate")
 
 
-def test_fp8_many_slots():
-    print("case: fp8 many slots", flush=True)
-    w = W.random_case(206, R=1, Mq=1, H=128, P=1200, NB=1100, K=1100, sigma=0.5).to_fp8()
+@pytest.mark.parametrize("shared", [True, False])
+def test_fp8_many_slots(shared):
+    print(f"case: fp8 many slots shared={shared}", flush=True)
+    w = W.random_case(206, R=1, Mq=1, H=128, P=1200, NB=1100, K=1100, sigma=0.5).to_fp8(shared)
     for s in (1, 0):
         _check(w, s, f"fp8 many slots splits={s}")
 

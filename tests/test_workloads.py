@@ -59,6 +59,27 @@ def test_block_quantisation_scale_and_error():
         assert np.all(err <= np.maximum(np.abs(x[b]) * 2.0 ** -4, 2.0 ** -10 * scales[b]) + 1e-30)
 
 
+def test_shared_block_scale_covers_both_pools():
+    """One scale per block for the 576-wide entries: absmax over ckv and kpe."""
+    w = W.random_case(6, R=1, Mq=1, H=1, P=4, NB=4, K=1, sigma=0.5)
+    kpe = w.kpe.copy()
+    kpe[2] = W.f32_to_bf16_bits(np.full((64, 64), 7.5, np.float32))  # kpe dominates block 2
+    c_codes, k_codes, scales = W.quantize_blocks_e4m3fn(w.ckv, kpe)
+    xc = W.bf16_bits_to_f32(w.ckv).astype(np.float64)
+    xk = W.bf16_bits_to_f32(kpe).astype(np.float64)
+    for b in range(4):
+        amax = max(np.abs(xc[b]).max(), np.abs(xk[b]).max())
+        assert scales[b] == np.float32(amax / np.float32(448.0))
+    assert scales[2] == np.float32(7.5 / 448.0)
+    only_c, s_c = W.quantize_blocks_e4m3fn(w.ckv)
+    assert np.array_equal(c_codes[[0, 1, 3]], only_c[[0, 1, 3]]) or not np.array_equal(
+        scales[[0, 1, 3]], s_c[[0, 1, 3]])
+    f = w.to_fp8()
+    assert f.kpe_scale is f.ckv_scale
+    g = w.to_fp8(shared_scale=False)
+    assert g.kpe_scale is not g.ckv_scale
+
+
 def test_config_structure_small():
     t = W.tiny()
     assert t.q_lat.shape == (1, 1, 16, 512) and t.ckv.shape == (4, 64, 512)
