@@ -131,10 +131,16 @@ def pin_bruteforce_multi(lib):
 
 
 def pin_bruteforce_fp8(lib):
-    w = W.random_case(12, R=2, Mq=1, H=3, P=5, NB=5, K=3, sigma=0.7).to_fp8()
-    out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
-                              w.ckv_scale, w.kpe_scale, lib=lib)
-    _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+    """Both scale layouts: one scale per block for the whole entry, and
+    separate latent and RoPE scales (which tells the two scales apart)."""
+    base = W.random_case(12, R=2, Mq=1, H=3, P=5, NB=5, K=3, sigma=0.7)
+    for shared in (True, False):
+        w = base.to_fp8(shared_scale=shared)
+        if not shared:
+            assert not np.array_equal(w.ckv_scale, w.kpe_scale)
+        out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                                  w.ckv_scale, w.kpe_scale, lib=lib)
+        _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
 
 
 # ------------------------------------------------------------ library special case
