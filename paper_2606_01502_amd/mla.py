@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import struct
 
 import torch
 
@@ -85,24 +86,30 @@ _TORCH_DTYPES = {
 }
 
 
+# mla_tensor_t packed field by field: data, dtype, ndim, shape[4], stride[4],
+# block_scale (88 bytes, no padding on x86-64)
+_PACK = struct.Struct("=Qii4q4qQ")
+assert _PACK.size == ctypes.sizeof(Tensor)
+_PAD = ((), (0,), (0, 0), (0, 0, 0), (0, 0, 0, 0))
+
+
 def describe(t: torch.Tensor | None, block_scale: torch.Tensor | None = None) -> Tensor | None:
     """mla_tensor_t for a torch tensor (uint8 tensors are fp8-e4m3fn codes)."""
     if t is None:
         return None
-    if t.dim() > 4:
+    shape, stride = t.shape, t.stride()
+    nd = len(shape)
+    if nd > 4:
         raise ValueError("at most 4 dims")
-    d = Tensor()
-    d.data = t.data_ptr() if t.numel() else None
-    d.dtype = _TORCH_DTYPES.get(t.dtype, 0)
-    d.ndim = t.dim()
-    for i in range(t.dim()):
-        d.shape[i] = t.shape[i]
-        d.stride[i] = t.stride(i)
+    bs = 0
     if block_scale is not None:
         if block_scale.dtype != torch.float32 or not block_scale.is_contiguous():
             raise ValueError("block_scale must be contiguous float32")
-        d.block_scale = block_scale.data_ptr()
-    return d
+        bs = block_scale.data_ptr()
+    pad = _PAD[4 - nd]
+    return Tensor.from_buffer_copy(_PACK.pack(t.data_ptr() if t.numel() else 0,
+                                              _TORCH_DTYPES.get(t.dtype, 0), nd, *shape, *pad,
+                                              *stride, *pad, bs))
 
 
 def _stream(stream):
@@ -120,6 +127,52 @@ def _ref(d):
     return ctypes.byref(d) if d is not None else None
 
 
+class _Prepared:
+    """One library call with its arguments fixed: the descriptors are built
+    once and the tensors they point to are kept alive, so each call costs
+    one foreign call (for serving loops that reuse static buffers)."""
+
+    def __init__(self, fn, args, keep, result):
+        self._fn, self._args, self._keep, self.result = fn, args, keep, result
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != MLA_OK:
+            raise MlaError(st, load().mla_last_error().decode())
+        return self.result
+
+
+def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
+                  out_lat, out_lse, ckv_scale, kpe_scale, n_splits, stream):
+    R, Mq, H, _ = q_lat.shape
+    if out_lat is None:
+        out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
+    if out_lse is None:
+        out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
+    opts = PartialOpts()
+    opts.n_splits = int(n_splits)
+    descs = (describe(q_lat), describe(q_pe), describe(ckv_pool, ckv_scale),
+             describe(kpe_pool, kpe_scale), describe(chunk_block_table), describe(sel_block_ids))
+    outs = (describe(out_lat), describe(out_lse))
+    args = tuple(_ref(d) for d in descs) + (ctypes.c_float(scale),) + \
+        tuple(_ref(d) for d in outs) + (ctypes.byref(opts), _stream(stream))
+    keep = (descs, outs, opts, q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
+            sel_block_ids, ckv_scale, kpe_scale)
+    return args, keep, (out_lat, out_lse)
+
+
+def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
+                    out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None, n_splits=0,
+                    stream=None):
+    """sparse_partial_attn with every argument fixed, the stream included
+    (the current one when None); calling the result launches the work and
+    returns (out_lat, out_lse)."""
+    args, keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
+                                       sel_block_ids, scale, out_lat, out_lse, ckv_scale,
+                                       kpe_scale, n_splits, stream)
+    return _Prepared(load().mla_sparse_partial_attn_ex, args, keep, result)
+
+
 def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
                         scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
                         n_splits=0, stream=None):
@@ -128,28 +181,14 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
     """
     lib = load()
-    R, Mq, H, _ = q_lat.shape
-    if out_lat is None:
-        out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
-    if out_lse is None:
-        out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
-    opts = PartialOpts()
-    opts.n_splits = int(n_splits)
-    st = lib.mla_sparse_partial_attn_ex(
-        _ref(describe(q_lat)), _ref(describe(q_pe)), _ref(describe(ckv_pool, ckv_scale)),
-        _ref(describe(kpe_pool, kpe_scale)), _ref(describe(chunk_block_table)),
-        _ref(describe(sel_block_ids)), ctypes.c_float(scale), _ref(describe(out_lat)),
-        _ref(describe(out_lse)), ctypes.byref(opts), _stream(stream))
-    _check(lib, st)
-    return out_lat, out_lse
+    args, _keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
+                                        sel_block_ids, scale, out_lat, out_lse, ckv_scale,
+                                        kpe_scale, n_splits, stream)
+    _check(lib, lib.mla_sparse_partial_attn_ex(*args))
+    return result
 
 
-def merge_partials(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
-    """LSE merge of partials (lists of [B, Mq, H, 512] / [B, Mq, H] fp32).
-
-    Returns out (and the merged lse when out_lse is given or requested by
-    passing out_lse=True)."""
-    lib = load()
+def _merge_args(parts_lat, parts_lse, out, out_lse, stream):
     n = len(parts_lat)
     if n != len(parts_lse):
         raise ValueError("parts_lat and parts_lse differ in length")
@@ -162,7 +201,25 @@ def merge_partials(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
     d_lse = [describe(t) for t in parts_lse]
     arr_lat = (ctypes.POINTER(Tensor) * max(n, 1))(*[ctypes.pointer(d) for d in d_lat])
     arr_lse = (ctypes.POINTER(Tensor) * max(n, 1))(*[ctypes.pointer(d) for d in d_lse])
-    st = lib.mla_merge_partials_ex(arr_lat, arr_lse, n, _ref(describe(out)),
-                                   _ref(describe(out_lse)) if want_lse else None, _stream(stream))
-    _check(lib, st)
-    return (out, out_lse) if want_lse else out
+    d_out = describe(out)
+    d_out_lse = describe(out_lse) if want_lse else None
+    args = (arr_lat, arr_lse, n, _ref(d_out), _ref(d_out_lse), _stream(stream))
+    keep = (d_lat, d_lse, d_out, d_out_lse, list(parts_lat), list(parts_lse))
+    return args, keep, ((out, out_lse) if want_lse else out)
+
+
+def prepare_merge(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
+    """merge_partials with every argument fixed (see prepare_partial)."""
+    args, keep, result = _merge_args(parts_lat, parts_lse, out, out_lse, stream)
+    return _Prepared(load().mla_merge_partials_ex, args, keep, result)
+
+
+def merge_partials(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
+    """LSE merge of partials (lists of [B, Mq, H, 512] / [B, Mq, H] fp32).
+
+    Returns out (and the merged lse when out_lse is given or requested by
+    passing out_lse=True)."""
+    lib = load()
+    args, _keep, result = _merge_args(parts_lat, parts_lse, out, out_lse, stream)
+    _check(lib, lib.mla_merge_partials_ex(*args))
+    return result

@@ -38,3 +38,32 @@ def test_descriptor_layout_matches_header():
     # void* + 2 x int32 + 4 x int64 + 4 x int64 + pointer
     assert ctypes.sizeof(mla.Tensor) == 8 + 8 + 32 + 32 + 8
     assert ctypes.sizeof(mla.PartialOpts) == 32
+
+
+def _describe_fieldwise(t, block_scale=None):
+    from paper_2606_01502_amd import mla
+    d = mla.Tensor()
+    d.data = t.data_ptr() if t.numel() else None
+    d.dtype = mla._TORCH_DTYPES.get(t.dtype, 0)
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.stride[i] = t.stride(i)
+    if block_scale is not None:
+        d.block_scale = block_scale.data_ptr()
+    return d
+
+
+def test_packed_descriptor_equals_fieldwise():
+    """describe() packs the struct in one go; it must give the same bytes as
+    setting each field of mla_tensor_t."""
+    import torch
+    from paper_2606_01502_amd import mla
+    base = torch.arange(4 * 6 * 5 * 8, dtype=torch.float32).reshape(4, 6, 5, 8)
+    scale = torch.ones(7, dtype=torch.float32)
+    cases = [(base, None), (base[1:3, ::2, :, 3:], None), (base.transpose(0, 2), None),
+             (torch.zeros(3, 64, 512, dtype=torch.uint8), scale),
+             (torch.zeros(5, 7, dtype=torch.int32), None), (torch.zeros(9, dtype=torch.bfloat16), None),
+             (torch.zeros(0, 4, dtype=torch.float32), None), (torch.zeros((), dtype=torch.float32), None)]
+    for t, bs in cases:
+        assert bytes(mla.describe(t, bs)) == bytes(_describe_fieldwise(t, bs)), (t.shape, t.stride())
