@@ -87,6 +87,11 @@ typedef struct {
  *                                            by the requester; no rotation here)
  *   ckv_pool          [P, 64, 512]    bf16 or fp8-e4m3fn (+block_scale), contiguous
  *   kpe_pool          [P, 64, 64]     same dtype as ckv_pool, contiguous
+ *                                     fp8: both descriptors carry a block_scale;
+ *                                     passing the same array for both (one scale
+ *                                     per block for the whole 576-wide entry) is
+ *                                     the fast layout, two arrays (separate
+ *                                     latent and RoPE scales) are also accepted
  *   chunk_block_table [R, NB] int32   logical block of job r's chunk -> pool block
  *   sel_block_ids     [R, K]  int32   selected logical blocks; -1 marks an empty
  *                                     slot; a block listed twice counts twice

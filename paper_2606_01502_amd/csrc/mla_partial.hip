@@ -31,9 +31,10 @@
 //
 // fp8 per-block scales (Section 6.3 mentions an FP8 sparse kernel; the scale
 // granularity is this library's) stay out of the bf16 tile, which holds the
-// codes exactly: the RoPE part of the scores is weighted by the RoPE / latent
-// scale ratio before the latent part is added, the scores by the latent
-// scale, and P by the latent scale before its bf16 rounding.
+// codes exactly: the scores are multiplied by the block's scale and P by the
+// same scale before its bf16 rounding.  With separate latent and RoPE scales
+// (the kKvFp8Split instance) the RoPE part of the scores is first weighted by
+// the RoPE / latent scale ratio, before the latent part is added.
 //
 // LDS swizzles (token t of the block, 16-byte chunk c of its row) are
 // described with bf16_key below.
