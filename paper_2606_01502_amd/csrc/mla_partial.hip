@@ -7,14 +7,14 @@
 // HBM once per workgroup and staged in LDS for all of its rows:
 //
 //   gather   direct-to-LDS 16-byte loads (global_load_lds_dwordx4) of each
-//            selected block into LDS, one block (bf16) or two (fp8) ahead of
-//            the block being computed.  The chunk's block table maps the
-//            selected logical block to its pool block.  bf16 blocks (64 KiB
-//            latent + 8 KiB RoPE rows) land directly in the compute layout;
-//            fp8 blocks (e4m3 codes, 36 KiB) land as they are and the
-//            workgroup converts them into a bf16 tile, exactly, once per block.
+//            selected block into LDS, one block (bf16, 72 KiB) or three (fp8
+//            e4m3 codes, 36 KiB) ahead of the block being computed.  The
+//            chunk's block table maps the selected logical block to its pool
+//            block.  Blocks land swizzled, in the layout the reads below use.
 //   S^T      = K . Q^T per wave for its 16*RG rows: bf16 MFMA 16x16x32, K read
-//            from LDS (b128), Q held in registers for the whole kernel.
+//            from LDS (16-byte reads of bf16, or 8-byte reads of e4m3 codes
+//            converted to bf16 in registers, exactly, between the products),
+//            Q held in registers for the whole kernel.
 //   softmax  online, in the exp2 domain, with wavefront reductions; the
 //            running max only moves when a block raises it by more than 2^8,
 //            so the accumulator is rarely rescaled (exact either way).
@@ -22,7 +22,8 @@
 //            bf16 MFMA with P^T taken straight from the S^T accumulator layout
 //            (the k index of the product is a fixed permutation of the block's
 //            tokens) and V^T read with the transposing LDS read
-//            (ds_read_b64_tr_b16) from the same tile, since the value is the
+//            (ds_read_b64_tr_b16, or ds_read_b64_tr_b8 and a conversion in
+//            registers for fp8) from the same stage, since the value is the
 //            latent part of the key (Section 3.2).  O lives in the
 //            accumulation registers for the whole kernel.
 //   epilogue normalised output and lse = max + ln(sum) per row, either to the
@@ -30,17 +31,19 @@
 //            combine kernel reduces with the merge algebra (Section 3.3).
 //
 // fp8 per-block scales (Section 6.3 mentions an FP8 sparse kernel; the scale
-// granularity is this library's) stay out of the bf16 tile, which holds the
+// granularity is this library's) stay out of the bf16 operands, which hold the
 // codes exactly: the scores are multiplied by the block's scale and P by the
 // same scale before its bf16 rounding.  With separate latent and RoPE scales
 // (the kKvFp8Split instance) the RoPE part of the scores is first weighted by
 // the RoPE / latent scale ratio, before the latent part is added.
 //
 // LDS swizzles (token t of the block, 16-byte chunk c of its row) are
-// described with bf16_key below.
+// described with bf16_key and fp8_key below.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "mla_kernels.h"
 
@@ -58,27 +61,25 @@ typedef int i32x2_t __attribute__((ext_vector_type(2)));
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
 
-// LDS layout.  bf16 caches: two stages, each one block in the compute layout
-// (64 latent rows of 1 KiB, then 64 RoPE rows of 128 B, swizzled as described
-// at bf16_key), loaded directly by the gather; block h+1 streams in while block
-// h is computed.  fp8 caches: one compute tile in the same bf16 layout, then
-// two stages holding a block's e4m3 codes as they lie in the pool (64 latent
-// rows of 512 B, then 64 RoPE rows of 64 B); at the start of a block the
-// workgroup converts its stage into the tile, and block h+2 streams in while
-// block h is computed.  After the stages: the compacted pool-block list of the
-// slot range and, for fp8, two floats per listed block (latent scale, RoPE /
-// latent scale ratio).
+// LDS layout.  bf16 caches: two stages of one block each (64 latent rows of
+// 1 KiB, then 64 RoPE rows of 128 B, swizzled as described at bf16_key);
+// block h+1 streams in while block h is computed.  fp8 caches: four stages of
+// one block of e4m3 codes each (64 latent rows of 512 B, then 64 RoPE rows of
+// 64 B, swizzled as described at fp8_key); blocks h+1 .. h+3 stream in while
+// block h is computed.  After the stages: the compacted pool-block list of
+// the slot range and, for fp8, two floats per listed block (latent scale,
+// RoPE / latent scale ratio).
 template <bool FP8>
 struct Layout {
-  static constexpr int kTile = kBlock * (kDLat + kDPe) * 2;  // 72 KiB
-  static constexpr int kTileCkv = kBlock * kDLat * 2;        // latent part of a tile
-  static constexpr int kStage = FP8 ? kBlock * (kDLat + kDPe) : kTile;
-  static constexpr int kStageCkv = FP8 ? kBlock * kDLat : kTileCkv;
-  static constexpr int kStageBase = FP8 ? kTile : 0;
-  static constexpr int kNum = 2;
-  static constexpr int kLead = FP8 ? 2 : 1;  // blocks streaming ahead of the computed one
+  static constexpr int kElt = FP8 ? 1 : 2;                     // bytes per element
+  static constexpr int kRow = kDLat * kElt;                    // latent row
+  static constexpr int kRopeRow = kDPe * kElt;                 // RoPE row
+  static constexpr int kStage = kBlock * (kRow + kRopeRow);    // 72 KiB or 36 KiB
+  static constexpr int kStageCkv = kBlock * kRow;
+  static constexpr int kNum = FP8 ? 4 : 2;
+  static constexpr int kLead = kNum - 1;  // blocks streaming ahead of the computed one
   static constexpr int kLoads = kStage / 1024 / 4;  // 1 KiB loads per wave per stage
-  static constexpr int kList = kStageBase + kNum * kStage;
+  static constexpr int kList = kNum * kStage;
   static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
   static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
   static constexpr int kTotal = kWaveCnt + 16;
@@ -220,6 +221,28 @@ MLA_STGROUP(1, 4, MLA_G14, MLA_OUT14, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
 #undef MLA_PRE
 #undef MLA_MFMA
 
+// Two S^T products sharing one query operand, c0 += a0 . q and c1 += a1 . q,
+// as one asm statement (the fp8 path issues a step as four of these with the
+// code conversions of the next step between them).  kFirst, kLast and kPre
+// as for StGroup.
+#define MLA_P2(C0, C1) "v_mfma_f32_16x16x32_bf16 %0, %2, %4, " C0 "\n\tv_mfma_f32_16x16x32_bf16 %1, %3, %4, " C1
+template <bool kFirst, bool kLast, bool kPre>
+__device__ __forceinline__ void st_pair(f32x4_t& c0, f32x4_t& c1, bf16x8_t a0, bf16x8_t a1, bf16x8_t q) {
+  if constexpr (kFirst) {
+    if constexpr (kPre)
+      asm("s_nop 2\n\t" MLA_P2("0", "0") : "=&v"(c0), "=&v"(c1) : "v"(a0), "v"(a1), "v"(q));
+    else
+      asm(MLA_P2("0", "0") : "=&v"(c0), "=&v"(c1) : "v"(a0), "v"(a1), "v"(q));
+  } else if constexpr (kLast) {
+    asm(MLA_P2("%0", "%1") "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
+  } else if constexpr (kPre) {
+    asm("s_nop 2\n\t" MLA_P2("%0", "%1") : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
+  } else {
+    asm(MLA_P2("%0", "%1") : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
+  }
+}
+#undef MLA_P2
+
 // x * s for an accumulator tile that lives in the accumulation registers.
 // The empty asm statements keep the tile there: without them the register
 // allocator moves part of O into architectural VGPRs for the whole kernel to
@@ -283,6 +306,16 @@ __device__ __forceinline__ int lds_opaque(int v) {
 // LDS traffic is not the limit.
 __device__ __forceinline__ int bf16_key(int t) { return t & 15; }
 
+// Swizzle keys of an fp8 stage (e4m3 codes as 512-byte latent rows and 64-byte
+// RoPE rows): 16-byte chunk c of latent row t sits in slot c ^ fp8_key(t),
+// chunk c of RoPE row t in slot c ^ fp8_rope_key(t).  The key reads (8 bytes,
+// 32 lanes per cycle: 16 tokens x both halves of one chunk) and the
+// transposing value reads (8 tokens {4G..4G+3, 16+4G..+3} per 16-lane group G,
+// 16 tokens per 32 lanes) then touch 16 distinct 16-byte bank groups, and the
+// RoPE key reads 16 distinct ones as well.
+__device__ __forceinline__ int fp8_key(int t) { return (t & 7) | ((((t >> 3) ^ (t >> 4)) & 1) << 3); }
+__device__ __forceinline__ int fp8_rope_key(int t) { return (t >> 2) & 3; }
+
 // Issue the direct-to-LDS loads of pool block b into a stage (Layout::kLoads
 // 1 KiB loads per wave).
 //   bf16: load j < 16 of wave w is latent row t = 16w + j (lane loads chunk
@@ -291,9 +324,12 @@ __device__ __forceinline__ int bf16_key(int t) { return t & 15; }
 //   fp8:  the stage is a plain copy: wave w loads latent bytes 8w .. 8w+7 KiB
 //         and RoPE bytes w .. w+1 KiB of the block.
 template <bool FP8>
-__device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, LDS uint8_t* buf,
+__device__ __forceinline__ void issue_stage(const PartialParams& p, int b_in, LDS uint8_t* buf,
                                             int wave, int lane_in) {
   using Ly = Layout<FP8>;
+  // the block id is the same in every lane; in scalar registers, the pool
+  // addresses below are scalar bases
+  const int64_t b = __builtin_amdgcn_readfirstlane(b_in);
   // Recompute the per-lane source offsets at every issue instead of letting
   // them be hoisted out of the main loop: registers are scarce there.
   int lane;
@@ -315,12 +351,19 @@ __device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, L
       dma16(kpe + t * 128 + (c << 4), buf + Ly::kStageCkv + k * 1024);
     }
   } else {
+    // load j of wave w: latent rows 2k, 2k+1 (k = 8w + j), lane -> row
+    // 2k + (lane >> 5), slot lane & 31; RoPE rows 16w .. 16w+15, lane -> row
+    // 16w + (lane >> 2), slot lane & 3
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int k = wave * 8 + j;
-      dma16s(ckv + k * 1024, lane16, buf + k * 1024);
+      const int t = 2 * k + (lane >> 5);
+      const uint32_t c = (uint32_t)((lane & 31) ^ fp8_key(t));
+      dma16s(ckv, (uint32_t)t * 512u + (c << 4), buf + k * 1024);
     }
-    dma16s(kpe + wave * 1024, lane16, buf + Ly::kStageCkv + wave * 1024);
+    const int t = 16 * wave + (lane >> 2);
+    const uint32_t c = (uint32_t)((lane & 3) ^ fp8_rope_key(t));
+    dma16s(kpe, (uint32_t)t * 64u + (c << 4), buf + Ly::kStageCkv + wave * 1024);
   }
 }
 
@@ -328,7 +371,9 @@ __device__ __forceinline__ void issue_stage(const PartialParams& p, int64_t b, L
 template <bool FP8>
 __device__ __forceinline__ void wait_stages(int stages) {
   constexpr int L = Layout<FP8>::kLoads;
-  if (stages >= 1)
+  if (stages >= 2)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * L));
+  else if (stages == 1)
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(L));
   else
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
@@ -345,36 +390,6 @@ __device__ __forceinline__ uint32_t e4m3x2_bf16(uint32_t w) {
 __device__ __forceinline__ bf16x8_t e4m3x8_bf16(uint32_t w0, uint32_t w1) {
   return __builtin_bit_cast(bf16x8_t, u32x4_t{e4m3x2_bf16<false>(w0), e4m3x2_bf16<true>(w0),
                                               e4m3x2_bf16<false>(w1), e4m3x2_bf16<true>(w1)});
-}
-
-// Convert a stage of e4m3 codes into the bf16 compute tile: 4608 units of 8
-// codes (64 latent rows x 64 units, then 64 RoPE rows x 8 units), 18 per lane.
-// In each round a wave converts 64 consecutive units: it reads 512 contiguous
-// bytes and writes one latent row (or 8 RoPE rows) of the tile.  The codes
-// are converted exactly (every e4m3 value is a bf16 value); the block scales
-// are applied to the products in fp32.
-__device__ __forceinline__ void convert_stage(const LDS uint8_t* st, LDS uint8_t* tile, int tid) {
-  constexpr int kCkvUnits = kBlock * kDLat / 8;
-  constexpr int kGroup = 3;  // rounds in flight (bounds the registers it takes)
-#pragma unroll
-  for (int it0 = 0; it0 < 18; it0 += kGroup) {
-    i32x2_t w[kGroup];
-#pragma unroll
-    for (int k = 0; k < kGroup; ++k) w[k] = *(const LDS i32x2_t*)(st + ((it0 + k) * 256 + tid) * 8);
-#pragma unroll
-    for (int k = 0; k < kGroup; ++k) {
-      const int it = it0 + k, u = it * 256 + tid;
-      const bf16x8_t v = e4m3x8_bf16((uint32_t)w[k][0], (uint32_t)w[k][1]);
-      if (it < 16) {
-        const int t = u >> 6, c = u & 63;
-        *(LDS bf16x8_t*)(tile + t * 1024 + ((c ^ bf16_key(t)) << 4)) = v;
-      } else {
-        const int ur = u - kCkvUnits, t = ur >> 3, c = ur & 7;
-        *(LDS bf16x8_t*)(tile + kBlock * 1024 + t * 128 + ((c ^ ((t >> 1) & 7)) << 4)) = v;
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
 }
 
 // Value fragments of O^T += V^T . P^T from a bf16 tile: fragment f = 32ps + dt
@@ -402,6 +417,27 @@ struct VFrags {
   }
 };
 
+// Value fragments from an fp8 stage: the same operand as VFrags, read with
+// the transposing 8-bit read (each 16-lane group reads 8 tokens x 16 columns;
+// lane i = 2r + q supplies token row r, bytes 8q .. 8q+7 of chunk dt) and
+// converted to bf16 in registers.  Token row r of group G is
+// tb = 4G + r (r < 4) or 16 + 4G + r - 4 of the k-step's 32 tokens, and
+// fp8_key(32ps + tb) = fp8_key(tb).
+struct VFrags8 {
+  const LDS uint8_t* cb;
+  int base;
+  __device__ __forceinline__ VFrags8(const LDS uint8_t* cb_, int lv) : cb(cb_) {
+    const int G = lv >> 4, i = lv & 15, r = i >> 1, q = i & 1;
+    const int tb = r < 4 ? 4 * G + r : 16 + 4 * G + (r - 4);
+    base = tb * 512 + 8 * q + (fp8_key(tb) << 4);
+  }
+  __device__ __forceinline__ i32x2_t raw(int f) const {
+    const int ps = f >> 5, dt = f & 31;
+    return __builtin_bit_cast(
+        i32x2_t, __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS i32x2_t*)(cb + ps * 16384 + (base ^ (dt << 4)))));
+  }
+};
+
 // RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
 // of the row tile (64*RG rows) over all 512 latent columns.  KV is the cache
 // kind: bf16, e4m3 with one scale per block for the whole 576-wide entries, or
@@ -417,7 +453,7 @@ void partial_kernel(const PartialParams p) {
   constexpr int kRowsWg = 64 * RG;
   __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
   LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
-  LDS uint8_t* const stage0 = smem + L::kStageBase;
+  LDS uint8_t* const stage0 = smem;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -529,17 +565,12 @@ void partial_kernel(const PartialParams p) {
     // the softmax scale times the latent scale; P is scaled by the latent
     // scale before its bf16 rounding.
     float s_mult = p.scale_log2, v_mult = 1.f, pe_ratio = 1.f;
-    const LDS uint8_t* cb;
     if constexpr (FP8) {
       v_mult = scales[2 * h];
       if constexpr (kSplitScales) pe_ratio = scales[2 * h + 1];
       s_mult = p.scale_log2 * v_mult;
-      convert_stage(stage0 + (h % L::kNum) * L::kStage, smem, tid);
-      lds_barrier();  // the tile is complete; every wave is done with the stage
-      cb = smem;
-    } else {
-      cb = stage0 + (h % L::kNum) * L::kStage;
     }
+    const LDS uint8_t* const cb = stage0 + (h % L::kNum) * L::kStage;
     // The next stage's loads, all at once, right after the first key reads of
     // this block (whose latency they cover).  Spreading them between the
     // products measured slower: the per-CU address unit takes about one 1 KiB
@@ -560,12 +591,32 @@ void partial_kernel(const PartialParams p) {
     // keep the compiler from regrouping loads next to their use.
     f32x4_t sacc[RG][kTau4];
     {
-      // Latent chunk 4ks+lg of token 16tau+ln16 sits in slot
+      // bf16: latent chunk 4ks+lg of token 16tau+ln16 sits in slot
       // (4ks+lg) ^ bf16_key(ln16) = 4ks ^ (lg ^ bf16_key(ln16)).
-      const int key_base = ln16 * 1024 + ((lg ^ bf16_key(ln16)) << 4);
-      const int rope_base = L::kTileCkv + ln16 * 128;
-      auto key_frags = [&](int step, bf16x8_t (&a)[kTau4]) {
-        if (step < 2) {
+      // fp8: the lane reads 8 codes, bytes 32ks + 8lg .. of the row = half
+      // (lg & 1) of chunk 2ks + (lg >> 1), slot (2ks + (lg >> 1)) ^ fp8_key(t)
+      // with fp8_key(16tau + n) = fp8_key(n) ^ (tau & 1) << 3; RoPE rows
+      // likewise with fp8_rope_key(16tau + n) = fp8_rope_key(n).
+      const int key_base = FP8 ? ln16 * 512 + 8 * (lg & 1) + (((lg >> 1) ^ fp8_key(ln16)) << 4)
+                               : ln16 * 1024 + ((lg ^ bf16_key(ln16)) << 4);
+      const int rope_base = FP8 ? L::kStageCkv + ln16 * 64 + 8 * (lg & 1) +
+                                      (((lg >> 1) ^ fp8_rope_key(ln16)) << 4)
+                                : L::kStageCkv + ln16 * 128;
+      // bf16: the ring holds operands; fp8: it holds codes, converted at use
+      using KRing = typename std::conditional<FP8, i32x2_t, bf16x8_t>::type;
+      auto key_frags = [&](int step, KRing (&a)[kTau4]) {
+        if constexpr (FP8) {
+          if (step < 2) {
+#pragma unroll
+            for (int tau = 0; tau < kTau4; ++tau)
+              a[tau] = *(const LDS i32x2_t*)(cb + tau * 1024 + (rope_base ^ (step << 5)));
+          } else {
+            const int ks = step - 2;
+#pragma unroll
+            for (int tau = 0; tau < kTau4; ++tau)
+              a[tau] = *(const LDS i32x2_t*)(cb + tau * 8192 + (key_base ^ ((ks << 5) ^ ((tau & 1) << 7))));
+          }
+        } else if (step < 2) {
 #pragma unroll
           for (int tau = 0; tau < kTau4; ++tau)
             a[tau] = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
@@ -576,22 +627,78 @@ void partial_kernel(const PartialParams p) {
             a[tau] = lds_b128(cb + tau * 16384 + (key_base ^ (ks << 6)));
         }
       };
-      bf16x8_t ka[3][kTau4];
-      key_frags(0, ka[0]);
-      key_frags(1, ka[1]);
+      auto key_ops = [&](const KRing (&r)[kTau4], bf16x8_t (&a)[kTau4]) {
+#pragma unroll
+        for (int tau = 0; tau < kTau4; ++tau) {
+          if constexpr (FP8) a[tau] = e4m3x8_bf16((uint32_t)r[tau][0], (uint32_t)r[tau][1]);
+          else a[tau] = r[tau];
+        }
+      };
+      // Codes are converted one step before their products: a VALU write of
+      // an operand is not interlocked against the products that read it, and
+      // a whole group of products lies between the two.  The first step's
+      // group leads with the wait states instead.
+      KRing kr[3][kTau4];
+      bf16x8_t ka[2][kTau4];
+      key_frags(0, kr[0]);
+      key_frags(1, kr[1]);
       issue_next();
+      key_ops(kr[0], ka[0]);
 #pragma unroll
       for (int step = 0; step < 18; ++step) {
-        if (step + 2 < 18) key_frags(step + 2, ka[(step + 2) % 3]);
+        if (step + 2 < 18) key_frags(step + 2, kr[(step + 2) % 3]);
+        if constexpr (FP8) {
+          // Four pairs of products; after pair j the codes of token tile j of
+          // the next step are converted (4 VALU ops beside the matrix core).
+          // Every converted operand is read at least two products later.
+          __builtin_amdgcn_sched_barrier(0);
+          const int ks = step < 2 ? 16 + step : step - 2;
+          const bf16x8_t(&a)[kTau4] = ka[step % 2];
+          if (kSplitScales && step == 2) {
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+              for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
+          }
+#pragma unroll
+          for (int j = 0; j < 2 * RG; ++j) {
+            const int rg = j >> 1, t0 = 2 * (j & 1);
+            f32x4_t& c0 = sacc[rg][t0];
+            f32x4_t& c1 = sacc[rg][t0 + 1];
+            const bf16x8_t q = qb[rg][ks];
+            const bool last = j == 2 * RG - 1;
+            if (step == 0)
+              st_pair<true, false, true>(c0, c1, a[t0], a[t0 + 1], q);
+            else if ((step == 17 || (kSplitScales && step == 1)) && last)
+              st_pair<false, true, false>(c0, c1, a[t0], a[t0 + 1], q);
+            else if (kSplitScales && step == 2 && j == 0)
+              st_pair<false, false, true>(c0, c1, a[t0], a[t0 + 1], q);
+            else
+              st_pair<false, false, false>(c0, c1, a[t0], a[t0 + 1], q);
+            __builtin_amdgcn_sched_barrier(0);
+            const int tc = j * kTau4 / (2 * RG);  // RG = 2: one tile per pair; RG = 1: two
+            if (step + 1 < 18) {
+#pragma unroll
+              for (int u = 0; u < kTau4 / (2 * RG); ++u) {
+                const KRing& w = kr[(step + 1) % 3][tc + u];
+                if constexpr (FP8) ka[(step + 1) % 2][tc + u] = e4m3x8_bf16((uint32_t)w[0], (uint32_t)w[1]);
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          continue;
+        }
+        if (step + 1 < 18) key_ops(kr[(step + 1) % 3], ka[(step + 1) % 2]);
+        const bf16x8_t (&ka_s)[kTau4] = ka[step % 2];
         __builtin_amdgcn_sched_barrier(0);
         const int ks = step < 2 ? 16 + step : step - 2;
         bf16x8_t q[RG];
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
         if (step == 0) {
-          StGroup<RG, kTau4, true, false, false>::run(sacc, ka[0], q);
+          StGroup<RG, kTau4, true, false, FP8>::run(sacc, ka_s, q);
         } else if (step == 17 || (kSplitScales && step == 1)) {
-          StGroup<RG, kTau4, false, true, false>::run(sacc, ka[step % 3], q);
+          StGroup<RG, kTau4, false, true, false>::run(sacc, ka_s, q);
         } else if (kSplitScales && step == 2) {
           // The RoPE part is complete: weight it by the scale ratio, in place;
           // the group's lead covers this VALU write of its accumulators.
@@ -599,9 +706,9 @@ void partial_kernel(const PartialParams p) {
           for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
             for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
-          StGroup<RG, kTau4, false, false, true>::run(sacc, ka[step % 3], q);
+          StGroup<RG, kTau4, false, false, true>::run(sacc, ka_s, q);
         } else {
-          StGroup<RG, kTau4, false, false, false>::run(sacc, ka[step % 3], q);
+          StGroup<RG, kTau4, false, false, false>::run(sacc, ka_s, q);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -612,9 +719,22 @@ void partial_kernel(const PartialParams p) {
     constexpr int kPvAhead = 8;
     constexpr int kFrags = 32 * kKSteps;
     const VFrags vf(cb, lds_opaque(lane));
-    bf16x8_t vr[kPvAhead + 1];
+    const VFrags8 vf8(cb, lds_opaque(lane));
+    // bf16: the ring holds operands; fp8: it holds codes (converted at use)
+    using VRing = typename std::conditional<FP8, i32x2_t, bf16x8_t>::type;
+    auto vload = [&](int f) -> VRing {
+      if constexpr (FP8) return vf8.raw(f); else return vf.load(f);
+    };
+    auto vop = [&](const VRing& x) -> bf16x8_t {
+      if constexpr (FP8) return e4m3x8_bf16((uint32_t)x[0], (uint32_t)x[1]); else return x;
+    };
+    VRing vr[kPvAhead + 1];
 #pragma unroll
-    for (int f = 0; f < kPvAhead; ++f) vr[f] = vf.load(f);
+    for (int f = 0; f < kPvAhead; ++f) vr[f] = vload(f);
+    // fp8: operands are converted two fragments ahead, after the products of
+    // a fragment, so that the conversion runs beside them and no product waits
+    // for a conversion just issued
+    bf16x8_t vc[3];
     __builtin_amdgcn_sched_barrier(0);
 
     f32x4_t acc[RG][kTau4];
@@ -687,15 +807,26 @@ void partial_kernel(const PartialParams p) {
     // software pipeline kPvAhead fragments deep.
 #pragma unroll
     for (int f = 0; f < kFrags; ++f) {
-      if (f + kPvAhead < kFrags) vr[(f + kPvAhead) % (kPvAhead + 1)] = vf.load(f + kPvAhead);
+      if (f + kPvAhead < kFrags) vr[(f + kPvAhead) % (kPvAhead + 1)] = vload(f + kPvAhead);
       if (f < 32 && f % kLateStride == 0) {
         const int i = f / kLateStride;
         p_pair(i >> 2, 2 + ((i >> 1) & 1), 2 * (i & 1));
       }
       __builtin_amdgcn_sched_barrier(0);
       const int ps = f >> 5, dt = f & 31;
+      if constexpr (FP8) {
+        if (f == 0) {
+          vc[0] = vop(vr[0]);
+          vc[1] = vop(vr[1]);
+        }
 #pragma unroll
-      for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(vr[f % (kPvAhead + 1)], pb[rg][ps], O[dt][rg]);
+        for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(vc[f % 3], pb[rg][ps], O[dt][rg]);
+        if (f + 2 < kFrags) vc[(f + 2) % 3] = vop(vr[(f + 2) % (kPvAhead + 1)]);
+      } else {
+        const bf16x8_t v = vop(vr[f % (kPvAhead + 1)]);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) O[dt][rg] = mfma(v, pb[rg][ps], O[dt][rg]);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
