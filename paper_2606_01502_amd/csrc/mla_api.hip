@@ -227,9 +227,12 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (opts && opts->n_splits > 0) {
       S = std::min<int64_t>(opts->n_splits, std::max<int64_t>(K, 1));
     } else {
+      // enough work items to cover the chip, but at least two slots per split:
+      // a split of one block costs more in fixed latency (its prologue,
+      // epilogue and share of the combine) than the block itself
       const int64_t units = R * row_tiles;
       S = std::max<int64_t>(1, (device_cus() + units - 1) / units);
-      S = std::min<int64_t>(S, std::max<int64_t>(K, 1));
+      S = std::min<int64_t>(S, std::max<int64_t>(K / 2, 1));
     }
     S = std::max<int64_t>(S, (K + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
     int64_t sps = std::max<int64_t>(1, (K + S - 1) / S);
