@@ -316,16 +316,18 @@ __device__ __forceinline__ int bf16_key(int t) { return t & 15; }
 __device__ __forceinline__ int fp8_key(int t) { return (t & 7) | ((((t >> 3) ^ (t >> 4)) & 1) << 3); }
 __device__ __forceinline__ int fp8_rope_key(int t) { return (t >> 2) & 3; }
 
-// Issue the direct-to-LDS loads of pool block b into a stage (Layout::kLoads
-// 1 KiB loads per wave).
+// Load j of the direct-to-LDS loads of pool block b into a stage
+// (Layout::kLoads 1 KiB loads per wave per block).
 //   bf16: load j < 16 of wave w is latent row t = 16w + j (lane loads chunk
 //         lane ^ bf16_key(t) of the row); loads 16, 17 are RoPE rows
 //         16w .. 16w+7 and 16w+8 .. 16w+15 (chunk c in slot c ^ ((t >> 1) & 7)).
-//   fp8:  the stage is a plain copy: wave w loads latent bytes 8w .. 8w+7 KiB
-//         and RoPE bytes w .. w+1 KiB of the block.
+//   fp8:  load j < 8 of wave w holds latent rows 2k, 2k+1 (k = 8w + j; lane ->
+//         row 2k + (lane >> 5), slot lane & 31, chunk slot ^ fp8_key(row));
+//         load 8 holds RoPE rows 16w .. 16w+15 (lane -> row 16w + (lane >> 2),
+//         slot lane & 3, chunk slot ^ fp8_rope_key(row)).
 template <bool FP8>
-__device__ __forceinline__ void issue_stage(const PartialParams& p, int b_in, LDS uint8_t* buf,
-                                            int wave, int lane_in) {
+__device__ __forceinline__ void issue_load(const PartialParams& p, int b_in, LDS uint8_t* buf,
+                                           int wave, int lane_in, int j) {
   using Ly = Layout<FP8>;
   // the block id is the same in every lane; in scalar registers, the pool
   // addresses below are scalar bases
@@ -334,37 +336,38 @@ __device__ __forceinline__ void issue_stage(const PartialParams& p, int b_in, LD
   // them be hoisted out of the main loop: registers are scarce there.
   int lane;
   asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
-  const uint32_t lane16 = (uint32_t)lane << 4;
   const uint8_t* ckv = p.ckv + b * Ly::kStageCkv;
   const uint8_t* kpe = p.kpe + b * (Ly::kStage - Ly::kStageCkv);
   if constexpr (!FP8) {
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    if (j < 16) {
       const int t = wave * 16 + j;
-      dma16s(ckv + t * 1024, lane16 ^ (uint32_t)(bf16_key(t) << 4), buf + t * 1024);
-    }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int k = wave * 2 + j;  // 1 KiB = RoPE rows 8k .. 8k+7
+      dma16s(ckv + t * 1024, ((uint32_t)lane << 4) ^ (uint32_t)(bf16_key(t) << 4), buf + t * 1024);
+    } else {
+      const int k = wave * 2 + (j - 16);  // 1 KiB = RoPE rows 8k .. 8k+7
       const int t = 8 * k + (lane >> 3);
       const int c = (lane & 7) ^ ((t >> 1) & 7);
       dma16(kpe + t * 128 + (c << 4), buf + Ly::kStageCkv + k * 1024);
     }
   } else {
-    // load j of wave w: latent rows 2k, 2k+1 (k = 8w + j), lane -> row
-    // 2k + (lane >> 5), slot lane & 31; RoPE rows 16w .. 16w+15, lane -> row
-    // 16w + (lane >> 2), slot lane & 3
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    if (j < 8) {
       const int k = wave * 8 + j;
       const int t = 2 * k + (lane >> 5);
       const uint32_t c = (uint32_t)((lane & 31) ^ fp8_key(t));
       dma16s(ckv, (uint32_t)t * 512u + (c << 4), buf + k * 1024);
+    } else {
+      const int t = 16 * wave + (lane >> 2);
+      const uint32_t c = (uint32_t)((lane & 3) ^ fp8_rope_key(t));
+      dma16s(kpe, (uint32_t)t * 64u + (c << 4), buf + Ly::kStageCkv + wave * 1024);
     }
-    const int t = 16 * wave + (lane >> 2);
-    const uint32_t c = (uint32_t)((lane & 3) ^ fp8_rope_key(t));
-    dma16s(kpe, (uint32_t)t * 64u + (c << 4), buf + Ly::kStageCkv + wave * 1024);
   }
+}
+
+// All loads of pool block b into a stage.
+template <bool FP8>
+__device__ __forceinline__ void issue_stage(const PartialParams& p, int b, LDS uint8_t* buf,
+                                            int wave, int lane) {
+#pragma unroll
+  for (int j = 0; j < Layout<FP8>::kLoads; ++j) issue_load<FP8>(p, b, buf, wave, lane, j);
 }
 
 // Wait until at most `stages` later stages of this wave's loads are in flight.
@@ -571,12 +574,15 @@ void partial_kernel(const PartialParams p) {
       s_mult = p.scale_log2 * v_mult;
     }
     const LDS uint8_t* const cb = stage0 + (h % L::kNum) * L::kStage;
-    // The next stage's loads, all at once, right after the first key reads of
-    // this block (whose latency they cover).  Spreading them between the
-    // products measured slower: the per-CU address unit takes about one 1 KiB
-    // load per 18 cycles and holds each issuing wave until it does.
+    // The next stage's loads.  bf16: two per S^T step over the first nine
+    // steps, beside the products (all 18 at once would hold the four waves
+    // for about 1.6k cycles at the per-CU address unit, which takes one 1 KiB
+    // load per ~16 cycles; at two per step the unit keeps up and the loads
+    // cost ~50 cycles each).  fp8 (9 loads): all at once after the first key
+    // reads.
+    LDS uint8_t* const next_buf = stage0 + (hn % L::kNum) * L::kStage;
     auto issue_next = [&]() {
-      if (b_next >= 0) issue_stage<FP8>(p, b_next, stage0 + (hn % L::kNum) * L::kStage, wave, lane);
+      if (b_next >= 0) issue_stage<FP8>(p, b_next, next_buf, wave, lane);
       __builtin_amdgcn_sched_barrier(0);
     };
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
@@ -642,7 +648,7 @@ void partial_kernel(const PartialParams p) {
       bf16x8_t ka[2][kTau4];
       key_frags(0, kr[0]);
       key_frags(1, kr[1]);
-      issue_next();
+      if constexpr (FP8) issue_next();
       key_ops(kr[0], ka[0]);
 #pragma unroll
       for (int step = 0; step < 18; ++step) {
@@ -690,6 +696,10 @@ void partial_kernel(const PartialParams p) {
         }
         if (step + 1 < 18) key_ops(kr[(step + 1) % 3], ka[(step + 1) % 2]);
         const bf16x8_t (&ka_s)[kTau4] = ka[step % 2];
+        if (step < 9 && b_next >= 0) {
+          issue_load<false>(p, b_next, next_buf, wave, lane, 2 * step);
+          issue_load<false>(p, b_next, next_buf, wave, lane, 2 * step + 1);
+        }
         __builtin_amdgcn_sched_barrier(0);
         const int ks = step < 2 ? 16 + step : step - 2;
         bf16x8_t q[RG];
