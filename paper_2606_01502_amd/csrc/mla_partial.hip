@@ -370,6 +370,33 @@ __device__ __forceinline__ void issue_stage(const PartialParams& p, int b, LDS u
   for (int j = 0; j < Layout<FP8>::kLoads; ++j) issue_load<FP8>(p, b, buf, wave, lane, j);
 }
 
+// The bf16 loads of one block with their per-block parts precomputed: the
+// scalar pool bases and LDS base of this wave's rows, and the lane's byte
+// offset.  Latent load j reads row t = 16w + j, whose key bf16_key(t) = j, at
+// lane offset (lane16 ^ j << 4) + j * 1024 = lane16 ^ (j << 4 | j << 10).
+struct Bf16Issue {
+  const uint8_t* ckv;  // row 16w of the block
+  const uint8_t* kpe;  // RoPE rows of the block
+  uint32_t m0;         // LDS address of row 16w of the stage
+  uint32_t lds_rope;   // LDS address of the stage's RoPE part + 2 KiB * w
+  __device__ __forceinline__ void load(const PartialParams& p, int j, int wave, int lane_in) const {
+    if (j < 16) {
+      const uint32_t off = ((uint32_t)lds_opaque(lane_in) << 4) ^ (uint32_t)((j << 4) | (j << 10));
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                   :: "v"(off), "s"(ckv), "s"(m0 + (uint32_t)j * 1024u) : "memory", "m0");
+    } else {
+      int lane;
+      asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
+      const int k = wave * 2 + (j - 16);
+      const int t = 8 * k + (lane >> 3);
+      const int c = (lane & 7) ^ ((t >> 1) & 7);
+      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_rope + (uint32_t)(j - 16) * 1024u);
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                   :: "v"((uint32_t)(t * 128 + (c << 4))), "s"(kpe), "s"(d) : "memory", "m0");
+    }
+  }
+};
+
 // Wait until at most `stages` later stages of this wave's loads are in flight.
 template <bool FP8>
 __device__ __forceinline__ void wait_stages(int stages) {
@@ -575,12 +602,19 @@ void partial_kernel(const PartialParams p) {
     }
     const LDS uint8_t* const cb = stage0 + (h % L::kNum) * L::kStage;
     // The next stage's loads.  bf16: two per S^T step over the first nine
-    // steps, beside the products (all 18 at once would hold the four waves
-    // for about 1.6k cycles at the per-CU address unit, which takes one 1 KiB
-    // load per ~16 cycles; at two per step the unit keeps up and the loads
-    // cost ~50 cycles each).  fp8 (9 loads): all at once after the first key
-    // reads.
+    // steps, beside the products, with the per-block address parts computed
+    // once (all 18 at once would hold the four waves for about 1.6k cycles at
+    // the per-CU address unit, which takes one 1 KiB load per ~16 cycles).
+    // fp8 (9 loads): all at once after the first key reads.
     LDS uint8_t* const next_buf = stage0 + (hn % L::kNum) * L::kStage;
+    Bf16Issue bi;
+    if constexpr (!FP8) {
+      const int64_t bn = b_next >= 0 ? b_next : 0;
+      bi.ckv = p.ckv + bn * 65536 + wave * 16384;
+      bi.kpe = p.kpe + bn * 8192;
+      bi.m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + (uint32_t)wave * 16384u);
+      bi.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + 65536u + (uint32_t)wave * 2048u);
+    }
     auto issue_next = [&]() {
       if (b_next >= 0) issue_stage<FP8>(p, b_next, next_buf, wave, lane);
       __builtin_amdgcn_sched_barrier(0);
@@ -697,8 +731,8 @@ void partial_kernel(const PartialParams p) {
         if (step + 1 < 18) key_ops(kr[(step + 1) % 3], ka[(step + 1) % 2]);
         const bf16x8_t (&ka_s)[kTau4] = ka[step % 2];
         if (step < 9 && b_next >= 0) {
-          issue_load<false>(p, b_next, next_buf, wave, lane, 2 * step);
-          issue_load<false>(p, b_next, next_buf, wave, lane, 2 * step + 1);
+          bi.load(p, 2 * step, wave, lane);
+          bi.load(p, 2 * step + 1, wave, lane);
         }
         __builtin_amdgcn_sched_barrier(0);
         const int ks = step < 2 ? 16 + step : step - 2;
