@@ -30,13 +30,15 @@ def _load(path=None):
     else:
         if _lib is not None:
             return _lib
-        if not os.path.exists(_build.LIB):
+        # (re)build when the library is missing or older than its source
+        if (not os.path.exists(_build.LIB)
+                or os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC)):
             _build.build()
         lib = ctypes.CDLL(_build.LIB)
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     lib.oracle_partial.restype = i32
     lib.oracle_partial.argtypes = [i32, i32, i32, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp,
-                                   vp, vp, dbl, vp, vp, i32]
+                                   vp, vp, i32, dbl, vp, vp, i32]
     lib.oracle_merge.restype = i32
     lib.oracle_merge.argtypes = [i32, i64, i32, vp, vp, vp, vp, i32]
     lib.oracle_bf16_to_f64.restype = dbl
@@ -74,7 +76,8 @@ def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=
     q_lat uint16 [R, Mq, H, 512] and q_pe uint16 [R, Mq, H, 64] hold bf16 bits;
     ckv [P, 64, 512] / kpe [P, 64, 64] hold bf16 bits (uint16) or e4m3fn codes
     (uint8, with float32 per-block scales ckv_scale / kpe_scale [P]);
-    table int32 [R, NB]; sel int32 [R, K] (-1 = empty slot).
+    table int32 [R, NB]; sel int32 [R, K] (one selection per job) or
+    [R, Mq, K] (one per query row); -1 = empty slot.
     Returns (out float64 [R, Mq, H, 512], lse float64 [R, Mq, H]).
     """
     lib = lib or _load()
@@ -97,13 +100,14 @@ def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=
     assert ckv.shape == (P, BLOCK, DLAT) and kpe.shape == (P, BLOCK, DPE)
     table = np.ascontiguousarray(table, dtype=np.int32)
     sel = np.ascontiguousarray(sel, dtype=np.int32)
-    NB, K = table.shape[1], sel.shape[1]
-    assert table.shape[0] == R and sel.shape[0] == R
+    NB, K = table.shape[1], sel.shape[-1]
+    per_row = sel.ndim == 3
+    assert table.shape[0] == R and sel.shape[0] == R and (not per_row or sel.shape[1] == Mq)
     out = np.zeros((R, Mq, H, DLAT), np.float64)
     lse = np.zeros((R, Mq, H), np.float64)
     rc = lib.oracle_partial(R, Mq, H, P, NB, K, _ptr(q_lat), _ptr(q_pe), kind, _ptr(ckv),
                             _ptr(kpe), _ptr(cs), _ptr(ks), _ptr(table), _ptr(sel),
-                            float(scale), _ptr(out), _ptr(lse),
+                            int(per_row), float(scale), _ptr(out), _ptr(lse),
                             int(n_threads or default_threads()))
     if rc != 0:
         raise ValueError("oracle_partial: invalid selected id or table entry")

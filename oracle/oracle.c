@@ -97,12 +97,15 @@ static double kpe_at(const kv_view* kv, int64_t b, int t, int d) {
  *   ckv [P][64][512], kpe [P][64][64]           bf16 bits, or e4m3fn codes
  *                                               with per-block scales
  *   table [R][NB]  logical block of the job's chunk -> pool block
- *   sel   [R][K]   selected logical blocks, -1 = empty slot; a block listed
- *                  twice is attended twice (multiset)
+ *   sel            selected logical blocks, -1 = empty slot; a block listed
+ *                  twice is attended twice (multiset).  sel_per_row = 0:
+ *                  [R][K], one selection for all rows of a job; 1:
+ *                  [R][Mq][K], a selection per query row (one holder serving
+ *                  several routed requesters on one chunk, Section 6.3)
  *   out   [R][Mq][H][512], lse [R][Mq][H]        double, written
  *
  * For job r and row (i, h), with T the multiset of tokens (b, t) of the
- * selected blocks:
+ * blocks selected for the row (by the job, or by query row i):
  *   s(b,t) = scale * (q_lat . ckv[b][t] + q_pe . kpe[b][t])
  *   lse    = ln sum_T exp(s)                    (via its maximum M)
  *   out    = sum_T exp(s - lse) * ckv[b][t]
@@ -115,16 +118,21 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
                    const uint16_t* q_lat, const uint16_t* q_pe, int kv_kind,
                    const void* ckv, const void* kpe, const float* ckv_scale,
                    const float* kpe_scale, const int32_t* table, const int32_t* sel,
-                   double scale, double* out, double* lse, int n_threads) {
+                   int sel_per_row, double scale, double* out, double* lse, int n_threads) {
   kv_view kv = {kv_kind, ckv, kpe, ckv_scale, kpe_scale};
   int bad = 0;
   if (kv_kind != ORACLE_KV_BF16 && kv_kind != ORACLE_KV_E4M3FN) return -1;
   if (kv_kind == ORACLE_KV_E4M3FN && (!ckv_scale || !kpe_scale)) return -1;
 
+  /* Row i of job r reads its selection at sel + r * sel_s0 + i * sel_s1. */
+  const int64_t sel_s1 = sel_per_row ? K : 0;
+  const int64_t sel_s0 = sel_per_row ? (int64_t)Mq * K : K;
+  const int n_sel = sel_per_row ? Mq : 1;
+
   /* Check every selected id and table entry before computing anything. */
   for (int r = 0; r < R; ++r)
-    for (int j = 0; j < K; ++j) {
-      int32_t s = sel[(int64_t)r * K + j];
+    for (int64_t jj = 0; jj < (int64_t)n_sel * K; ++jj) {
+      int32_t s = sel[(int64_t)r * sel_s0 + jj];
       if (s == -1) continue;
       if (s < 0 || s >= NB) return -1;
       int32_t b = table[(int64_t)r * NB + s];
@@ -135,14 +143,16 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
 #pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads) reduction(| : bad)
   for (int64_t row = 0; row < n_rows; ++row) {
     int r = (int)(row / ((int64_t)Mq * H));
+    int i = (int)((row / H) % Mq);
+    const int32_t* row_sel = sel + (int64_t)r * sel_s0 + (int64_t)i * sel_s1;
     const uint16_t* ql = q_lat + row * ORACLE_DLAT;
     const uint16_t* qp = q_pe + row * ORACLE_DPE;
     double* o = out + row * ORACLE_DLAT;
 
-    /* The token multiset of this job, in slot order. */
+    /* The token multiset of this row, in slot order. */
     int n_tok = 0;
     for (int j = 0; j < K; ++j)
-      if (sel[(int64_t)r * K + j] != -1) n_tok += ORACLE_BLOCK;
+      if (row_sel[j] != -1) n_tok += ORACLE_BLOCK;
     for (int d = 0; d < ORACLE_DLAT; ++d) o[d] = 0.0;
     if (n_tok == 0) {
       lse[row] = -INFINITY;
@@ -160,7 +170,7 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
     /* Pass 1: every score. */
     int n = 0;
     for (int j = 0; j < K; ++j) {
-      int32_t s = sel[(int64_t)r * K + j];
+      int32_t s = row_sel[j];
       if (s == -1) continue;
       int64_t b = table[(int64_t)r * NB + s];
       for (int t = 0; t < ORACLE_BLOCK; ++t) {

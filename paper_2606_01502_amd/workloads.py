@@ -314,27 +314,61 @@ def make(name, seed=None, **kw):
     return fn(**kw) if seed is None else fn(seed=seed, **kw)
 
 
+def _slot_ids(rs, NB, K, nv, allow_dup, pad_pattern, common=None, shared_frac=0.0):
+    """K slots holding nv sorted ids (the rest -1).  With a common set, each
+    id is taken from it with probability shared_frac (rows that overlap)."""
+    if allow_dup:
+        ids = rs.integers(0, NB, nv)
+    else:
+        ids = rs.choice(NB, nv, replace=False)
+    if common is not None and nv:
+        take = rs.random(nv) < shared_frac
+        pick = rs.choice(common, nv, replace=True)
+        ids = np.where(take, pick, ids)
+        if not allow_dup:
+            ids = np.unique(ids)
+            extra = np.setdiff1d(np.arange(NB), ids)
+            if ids.size < nv:
+                ids = np.concatenate([ids, rs.choice(extra, nv - ids.size, replace=False)])
+    ids = np.sort(ids)
+    row = np.full(K, -1, np.int32)
+    if pad_pattern == "interleaved" and nv < K:
+        row[np.sort(rs.choice(K, nv, replace=False))] = ids
+    else:
+        row[:nv] = ids
+    return row
+
+
 def random_case(seed, R, Mq, H, P, NB, K, n_valid=None, sigma=1.0, allow_dup=False,
-                pad_pattern="tail"):
+                pad_pattern="tail", per_row=False, shared_frac=0.5):
     """Small random case for tests: R jobs over a P-block pool, NB logical
     blocks per job, K slots of which n_valid[r] hold ids.  pad_pattern is
-    'tail' (ids first), 'interleaved' (empty slots spread) or 'none'."""
+    'tail' (ids first), 'interleaved' (empty slots spread) or 'none'.
+    per_row gives every query row its own selection, sel [R, Mq, K], drawing
+    each id from a per-job common set with probability shared_frac so that
+    rows overlap; n_valid may then be [R][Mq]."""
     q_lat, q_pe = _queries(seed, R, Mq, H, sigma)
     ckv, kpe = _pool(seed, P, sigma)
     rng = np.random.default_rng([seed, _T_TABLE])
     table = np.stack([rng.choice(P, NB, replace=NB > P) for _ in range(R)]).astype(np.int32)
     rs = np.random.default_rng([seed, _T_SEL])
-    sel = np.full((R, K), -1, np.int32)
-    for r in range(R):
-        nv = K if n_valid is None else (n_valid[r] if np.ndim(n_valid) else n_valid)
-        if allow_dup:
-            ids = np.sort(rs.integers(0, NB, nv))
-        else:
-            ids = np.sort(rs.choice(NB, nv, replace=False))
-        if pad_pattern == "interleaved" and nv < K:
-            slots = np.sort(rs.choice(K, nv, replace=False))
-            sel[r, slots] = ids
-        else:
-            sel[r, :nv] = ids
+
+    def nvalid(r, i=None):
+        if n_valid is None:
+            return K
+        v = n_valid[r] if np.ndim(n_valid) else n_valid
+        return v[i] if (i is not None and np.ndim(v)) else v
+
+    if per_row:
+        sel = np.full((R, Mq, K), -1, np.int32)
+        for r in range(R):
+            common = rs.choice(NB, min(NB, K), replace=False)
+            for i in range(Mq):
+                sel[r, i] = _slot_ids(rs, NB, K, nvalid(r, i), allow_dup, pad_pattern, common,
+                                      shared_frac)
+    else:
+        sel = np.full((R, K), -1, np.int32)
+        for r in range(R):
+            sel[r] = _slot_ids(rs, NB, K, nvalid(r), allow_dup, pad_pattern)
     return Workload(f"random-{seed}", q_lat, q_pe, ckv, kpe, table, sel,
                     n_requests=R, merge_parts=1)

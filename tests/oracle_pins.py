@@ -70,7 +70,7 @@ def brute_force(w, rows=None):
     cache_v = {}
     for (r, i, h) in rows:
         toks = []
-        for s in w.sel[r]:
+        for s in (w.sel[r, i] if w.sel.ndim == 3 else w.sel[r]):
             if s < 0:
                 continue
             b = int(w.table[r, s])
@@ -141,6 +141,32 @@ def pin_bruteforce_fp8(lib):
         out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
                                   w.ckv_scale, w.kpe_scale, lib=lib)
         _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
+def pin_bruteforce_per_row(lib):
+    """A selection per query row (one holder serving several requesters on
+    one chunk): overlapping rows, duplicates, interleaved empty slots, and a
+    row with nothing selected."""
+    w = W.random_case(13, R=2, Mq=3, H=2, P=9, NB=6, K=4, n_valid=[[3, 0, 4], [4, 2, 1]],
+                      allow_dup=True, pad_pattern="interleaved", per_row=True)
+    assert w.sel.ndim == 3 and not all(np.array_equal(w.sel[0, 0], w.sel[0, i]) for i in range(3))
+    out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, lib=lib)
+    _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
+def pin_per_row_is_one_job_per_row(lib):
+    """Per-row selections equal the shared-selection form with every query
+    row routed as a job of its own (Mq = 1) on the same chunk."""
+    w = W.random_case(14, R=2, Mq=4, H=3, P=12, NB=8, K=5, allow_dup=True, per_row=True,
+                      shared_frac=0.7)
+    out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, lib=lib)
+    R, Mq, H, _ = w.q_lat.shape
+    q_lat = w.q_lat.reshape(R * Mq, 1, H, DLAT)
+    q_pe = w.q_pe.reshape(R * Mq, 1, H, DPE)
+    table = np.repeat(w.table, Mq, axis=0)
+    sel = w.sel.reshape(R * Mq, -1)
+    o2, l2 = oracle.partial(q_lat, q_pe, w.ckv, w.kpe, table, sel, w.scale, lib=lib)
+    assert np.array_equal(out.reshape(o2.shape), o2) and np.array_equal(lse.reshape(l2.shape), l2)
 
 
 # ------------------------------------------------------------ library special case
@@ -401,6 +427,7 @@ def pin_e4m3_decode(lib):
 
 
 ALL_PINS = [pin_bf16_decode, pin_e4m3_decode, pin_bruteforce_tiny, pin_bruteforce_multi,
+            pin_bruteforce_per_row, pin_per_row_is_one_job_per_row,
             pin_bruteforce_fp8, pin_dense_equals_library, pin_identical_tokens,
             pin_identical_keys_mean, pin_zero_query, pin_two_groups, pin_one_hot,
             pin_empty_and_duplicates, pin_merge_partition, pin_merge_algebra,

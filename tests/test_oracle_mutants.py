@@ -27,6 +27,9 @@ MUTANTS = [
     ("log2_lse", "double L = M + log(l);", "double L = M + log2(l);"),
     ("unnormalised_weights", "double w = exp(score[k] - L);", "double w = exp(score[k] - M);"),
     ("skip_block_table", "int64_t b = table[(int64_t)r * NB + s];", "int64_t b = s;"),
+    ("per_row_reads_row0",
+     "const int32_t* row_sel = sel + (int64_t)r * sel_s0 + (int64_t)i * sel_s1;",
+     "const int32_t* row_sel = sel + (int64_t)r * sel_s0;"),
     ("ckv_transposed", "int64_t i = (b * ORACLE_BLOCK + t) * ORACLE_DLAT + d;",
      "int64_t i = (b * ORACLE_DLAT + d) * ORACLE_BLOCK + t;"),
     ("value_wrong_token", "o[d] += w * ckv_at(&kv, blk[k], tok[k], d);",
