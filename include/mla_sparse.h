@@ -95,11 +95,23 @@ typedef struct {
  *   chunk_block_table [R, NB] int32   logical block of job r's chunk -> pool block
  *   sel_block_ids     [R, K]  int32   selected logical blocks; -1 marks an empty
  *                                     slot; a block listed twice counts twice
+ *                 or  [R, Mq, K] int32   one selection per query row: a holder
+ *                                     serving Mq routed requesters (or query
+ *                                     rows) on the job's chunk, each with its
+ *                                     own selection (Section 6.3).  Blocks that
+ *                                     several rows select are read once for
+ *                                     all of them.  bf16 caches only
+ *                                     (MLA_ERR_UNSUPPORTED for fp8); NB times
+ *                                     the query rows one row tile spans (128
+ *                                     rows, or 64 when 128 would span more
+ *                                     than 64 query rows) must not exceed
+ *                                     73728 (MLA_ERR_UNSUPPORTED)
  *   scale                              multiplies q_lat.ckv + q_pe.kpe
  *   out_lat           [R, Mq, H, 512] fp32   written: normalised partial output
  *   out_lse           [R, Mq, H]      fp32   written: natural-log log-sum-exp
  *
- * For each row, with T the multiset of tokens of the selected blocks,
+ * For each row, with T the multiset of tokens of the blocks selected for it
+ * (by its job, or by its query row),
  *   s_t = scale * (q_lat . ckv_t + q_pe . kpe_t),
  *   out_lse = ln sum_T exp(s_t),   out_lat = sum_T exp(s_t - out_lse) * ckv_t,
  * and for an empty T: out_lat = 0, out_lse = -inf.  No mask, no positions.

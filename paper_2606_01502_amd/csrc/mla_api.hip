@@ -164,7 +164,9 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (fp8 && (!ckv_pool->block_scale || !kpe_pool->block_scale))
       return fail(MLA_ERR_INVALID_ARGUMENT, "fp8 pools need block_scale");
     if ((st = check_tensor(chunk_block_table, "chunk_block_table", MLA_DTYPE_INT32, 2)) != MLA_OK) return st;
-    if ((st = check_tensor(sel_block_ids, "sel_block_ids", MLA_DTYPE_INT32, 2)) != MLA_OK) return st;
+    const bool per_row = sel_block_ids && sel_block_ids->ndim == 3;
+    if ((st = check_tensor(sel_block_ids, "sel_block_ids", MLA_DTYPE_INT32, per_row ? 3 : 2)) != MLA_OK)
+      return st;
     if ((st = check_tensor(out_lat, "out_lat", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
     if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
     if (opts) {
@@ -175,7 +177,7 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
 
     const int64_t R = q_lat->shape[0], Mq = q_lat->shape[1], H = q_lat->shape[2];
     const int64_t P = ckv_pool->shape[0];
-    const int64_t NB = chunk_block_table->shape[1], K = sel_block_ids->shape[1];
+    const int64_t NB = chunk_block_table->shape[1], K = sel_block_ids->shape[per_row ? 2 : 1];
     auto shape_is = [](const mla_tensor_t* t, std::initializer_list<int64_t> s) {
       int d = 0;
       for (int64_t v : s)
@@ -187,7 +189,10 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (!shape_is(ckv_pool, {P, MLA_BLOCK, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool: shape must be [P, 64, 512]");
     if (!shape_is(kpe_pool, {P, MLA_BLOCK, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "kpe_pool: shape must be [P, 64, 64] with the P of ckv_pool");
     if (chunk_block_table->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_block_table: shape must be [R, NB]");
-    if (sel_block_ids->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K]");
+    if (sel_block_ids->shape[0] != R || (per_row && sel_block_ids->shape[1] != Mq))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K] or [R, Mq, K]");
+    if (per_row && fp8)
+      return fail(MLA_ERR_UNSUPPORTED, "per-row selections need a bf16 cache");
     if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
     if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
     if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||
@@ -220,7 +225,26 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
 
     // ---- plan: row tiles of 128 or 64 rows (4 waves of 32 or 16 rows);
     // split-K over slot ranges so that the grid covers the chip
-    const int row_groups = rows > 64 ? 2 : 1;
+    int row_groups = rows > 64 ? 2 : 1;
+    // per-row selections: the query rows a row tile spans (one mask bit each)
+    auto tile_query_rows = [&](int rg) {
+      const int64_t rw = 64 * rg;
+      int64_t most = 0;
+      for (int64_t r0 = 0; r0 < rows; r0 += rw) {
+        const int64_t last = std::min<int64_t>(r0 + rw, rows) - 1;
+        most = std::max<int64_t>(most, last / H - r0 / H + 1);
+      }
+      return most;
+    };
+    int64_t tile_qrows = 1;
+    if (per_row) {
+      if (row_groups == 2 && tile_query_rows(2) > mla::kPerRowMaxRows) row_groups = 1;
+      tile_qrows = tile_query_rows(row_groups);
+      if (tile_qrows > mla::kPerRowMaxRows)
+        return fail(MLA_ERR_UNSUPPORTED, "per-row selections: too many query rows per tile");
+      if (NB * tile_qrows * 2 > mla::kPerRowCounterBytes)
+        return fail(MLA_ERR_UNSUPPORTED, "per-row selections: NB x query rows per tile too large");
+    }
     const int rows_wg = 64 * row_groups;
     const int64_t row_tiles = (rows + rows_wg - 1) / rows_wg;
     int64_t S;
@@ -234,8 +258,11 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       S = std::max<int64_t>(1, (device_cus() + units - 1) / units);
       S = std::min<int64_t>(S, std::max<int64_t>(K / 2, 1));
     }
-    S = std::max<int64_t>(S, (K + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
+    // a split's block list holds at most kMaxSlotsPerSplit entries: its slots,
+    // or for per-row selections its slots of every query row of the tile
+    S = std::max<int64_t>(S, (K * tile_qrows + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
     int64_t sps = std::max<int64_t>(1, (K + S - 1) / S);
+    if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, mla::kMaxSlotsPerSplit / tile_qrows));
     S = std::max<int64_t>(1, (K + sps - 1) / sps);
     if (R * row_tiles * S > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "grid too large");
 
@@ -253,6 +280,7 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     p.table_s0 = chunk_block_table->stride[0];
     p.sel = (const int32_t*)sel_block_ids->data;
     p.sel_s0 = sel_block_ids->stride[0];
+    p.sel_s1 = per_row ? sel_block_ids->stride[1] : 0;
     p.P = P;
     p.NB = (int32_t)NB;
     p.K = (int32_t)K;
@@ -278,7 +306,7 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     const int kv = !fp8 ? mla::kKvBf16
                  : (ckv_pool->block_scale == kpe_pool->block_scale ? mla::kKvFp8Shared
                                                                    : mla::kKvFp8Split);
-    hipError_t e = mla::launch_partial(p, (int)R, kv, row_groups, hs);
+    hipError_t e = mla::launch_partial(p, (int)R, kv, row_groups, per_row, hs);
     if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
     if (S > 1) {
       mla::CombineParams c{};

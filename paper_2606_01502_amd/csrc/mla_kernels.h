@@ -28,6 +28,7 @@ struct PartialParams {
   int64_t table_s0;
   const int32_t* sel;
   int64_t sel_s0;
+  int64_t sel_s1;  // stride over query rows i: 0 when one selection serves the whole job
   int64_t P;
   int32_t NB, K;
   int32_t Mq, H, rows;  // rows = Mq * H
@@ -72,9 +73,16 @@ constexpr int kKvBf16 = 0;
 constexpr int kKvFp8Shared = 1;  // e4m3, one scale per block for ckv and kpe
 constexpr int kKvFp8Split = 2;   // e4m3, separate ckv and kpe scales per block
 
+// Per-row selections: the LDS counters of one workgroup's compaction live in
+// its stage area, NB * (query rows of the tile) 16-bit counters.
+constexpr int kPerRowCounterBytes = 2 * 64 * 1152;  // the bf16 stage area
+constexpr int kPerRowMaxRows = 64;                  // query rows per row tile (mask bits)
+
 // Launchers; return hipSuccess or the launch error.
-// row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows)
-hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, hipStream_t s);
+// row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows);
+// per_row: sel holds a selection per query row (bf16 caches only)
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, bool per_row,
+                          hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_merge(const MergeParams& p, hipStream_t s);
 

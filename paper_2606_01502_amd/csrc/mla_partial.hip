@@ -82,10 +82,14 @@ struct Layout {
   static constexpr int kList = kNum * kStage;
   static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
   static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
-  static constexpr int kTotal = kWaveCnt + 16;
+  static constexpr int kMasks = kWaveCnt + 16;  // per-row selections: 64-bit row mask per entry
+  static constexpr int kTotal = kMasks;
+  static constexpr int kTotalPerRow = kMasks + kMaxSlotsPerSplit * 8;
 };
-static_assert(Layout<true>::kTotal <= 160 * 1024 && Layout<false>::kTotal <= 160 * 1024,
+static_assert(Layout<true>::kTotal <= 160 * 1024 && Layout<false>::kTotalPerRow <= 160 * 1024,
               "LDS budget");
+static_assert(kPerRowCounterBytes <= Layout<false>::kNum * Layout<false>::kStage,
+              "per-row counters live in the stage area");
 constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -468,38 +472,15 @@ struct VFrags8 {
   }
 };
 
-// RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
-// of the row tile (64*RG rows) over all 512 latent columns.  KV is the cache
-// kind: bf16, e4m3 with one scale per block for the whole 576-wide entries, or
-// e4m3 with separate latent and RoPE scales per block.
-template <int RG, int KV>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void partial_kernel(const PartialParams p) {
-  constexpr bool FP8 = KV != kKvBf16;
-  constexpr bool kSplitScales = KV == kKvFp8Split;
+// Compact the valid selected blocks of slots [slot0, slot0 + nslots) of job r
+// into the LDS list (slot order kept); for fp8 also each listed block's latent
+// scale and RoPE / latent scale ratio.  Returns the number of listed blocks.
+template <bool FP8>
+__device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int slot0, int nslots,
+                                             LDS uint8_t* smem, int tid) {
   using L = Layout<FP8>;
-  constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
-  constexpr int kKSteps = kBlock / 32;  // 32-token PV k-steps per block
-  constexpr int kRowsWg = 64 * RG;
-  __shared__ __attribute__((aligned(16))) uint8_t smem_raw[L::kTotal];
-  LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
-  LDS uint8_t* const stage0 = smem;
-
-  const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n16 = lane & 15;  // MFMA column / row-in-group index
-  const int g = lane >> 4;    // MFMA k-group
-
-  // ---- work item
-  const int w_id = blockIdx.x;
-  const int s_idx = w_id % p.n_splits;
-  const int rt = (w_id / p.n_splits) % p.row_tiles;
-  const int r = w_id / (p.n_splits * p.row_tiles);
-  const int slot0 = s_idx * p.slots_per_split;
-  const int nslots = max(0, min(p.K - slot0, p.slots_per_split));
-
-  // ---- compact the valid selected blocks of the slot range (slot order kept)
   LDS int* list = (LDS int*)(smem + L::kList);
   LDS float* scales = (LDS float*)(smem + L::kScales);
   LDS int* wave_cnt = (LDS int*)(smem + L::kWaveCnt);
@@ -535,6 +516,125 @@ void partial_kernel(const PartialParams p) {
     }
     n_valid += total;
     lds_barrier();
+  }
+  return n_valid;
+}
+
+// Per-row selections: compact the blocks that query rows i0 .. i0 + n_i - 1
+// of job r select in slots [slot0, slot0 + nslots) into the LDS list, each
+// block once per copy, with a mask of the rows that hold that copy: a block
+// that row i lists c_i times gives max_i c_i entries, entry k carrying the
+// rows with c_i > k.  Each row thus attends exactly its own multiset, and a
+// block that several rows chose is loaded once for all of them.  Entries
+// come in ascending logical-block order.  The counters (16 bits per (block,
+// row); at most nslots each) use the stage area, which is free until the
+// first load is issued.  Returns the number of entries.
+__device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, int slot0,
+                                               int nslots, int i0, int n_i, LDS uint8_t* smem,
+                                               LDS int* list, LDS uint64_t* masks, int tid) {
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  LDS uint32_t* cnt = (LDS uint32_t*)smem;
+  LDS const uint16_t* cnt16 = (LDS const uint16_t*)smem;
+  LDS int* wave_cnt = (LDS int*)(smem + Layout<false>::kWaveCnt);
+  const int n_words = (p.NB * n_i + 1) >> 1;
+  for (int w = tid; w < n_words; w += 256) cnt[w] = 0u;
+  lds_barrier();
+  const int n_ent = n_i * nslots;
+  for (int e = tid; e < n_ent; e += 256) {
+    const int ii = e / nslots, j = e - ii * nslots;
+    const int id = p.sel[r * p.sel_s0 + (int64_t)(i0 + ii) * p.sel_s1 + slot0 + j];
+    if (id >= 0 && id < p.NB) {
+      const int bb = p.table[r * p.table_s0 + id];
+      if (bb >= 0 && bb < p.P) {
+        const int c = id * n_i + ii;
+        __atomic_fetch_add(&cnt[c >> 1], 1u << ((c & 1) * 16), __ATOMIC_RELAXED);
+      }
+    }
+  }
+  lds_barrier();
+  int n_valid = 0;
+  for (int base = 0; base < p.NB; base += 256) {
+    const int id = base + tid;
+    int kmax = 0;
+    if (id < p.NB)
+      for (int ii = 0; ii < n_i; ++ii) kmax = max(kmax, (int)cnt16[id * n_i + ii]);
+    // exclusive prefix sum of kmax over the workgroup (ascending id)
+    int incl = kmax;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    if (lane == 63) wave_cnt[wave] = incl;
+    lds_barrier();
+    int off = n_valid + incl - kmax, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = wave_cnt[w];
+      off += (w < wave) ? c : 0;
+      total += c;
+    }
+    if (kmax > 0) {
+      const int bb = p.table[r * p.table_s0 + id];
+      for (int k = 0; k < kmax; ++k) {
+        uint64_t m = 0;
+        for (int ii = 0; ii < n_i; ++ii)
+          if ((int)cnt16[id * n_i + ii] > k) m |= 1ull << ii;
+        list[off + k] = bb;
+        masks[off + k] = m;
+      }
+    }
+    n_valid += total;
+    lds_barrier();
+  }
+  return n_valid;
+}
+
+// RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
+// of the row tile (64*RG rows) over all 512 latent columns.  KV is the cache
+// kind: bf16, e4m3 with one scale per block for the whole 576-wide entries, or
+// e4m3 with separate latent and RoPE scales per block.
+template <int RG, int KV, bool PR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void partial_kernel(const PartialParams p) {
+  constexpr bool FP8 = KV != kKvBf16;
+  static_assert(!(PR && FP8), "per-row selections: bf16 caches only");
+  constexpr bool kSplitScales = KV == kKvFp8Split;
+  using L = Layout<FP8>;
+  constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
+  constexpr int kKSteps = kBlock / 32;  // 32-token PV k-steps per block
+  constexpr int kRowsWg = 64 * RG;
+  __shared__ __attribute__((aligned(16))) uint8_t smem_raw[PR ? L::kTotalPerRow : L::kTotal];
+  LDS uint8_t* smem = (LDS uint8_t*)smem_raw;
+  LDS uint8_t* const stage0 = smem;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n16 = lane & 15;  // MFMA column / row-in-group index
+  const int g = lane >> 4;    // MFMA k-group
+
+  // ---- work item
+  const int w_id = blockIdx.x;
+  const int s_idx = w_id % p.n_splits;
+  const int rt = (w_id / p.n_splits) % p.row_tiles;
+  const int r = w_id / (p.n_splits * p.row_tiles);
+  const int slot0 = s_idx * p.slots_per_split;
+  const int nslots = max(0, min(p.K - slot0, p.slots_per_split));
+
+  // ---- compact the valid selected blocks of the slot range (slot order kept;
+  // per-row selections: the union over the tile's query rows, with row masks)
+  LDS int* list = (LDS int*)(smem + L::kList);
+  LDS float* scales = (LDS float*)(smem + L::kScales);
+  LDS uint64_t* masks = (LDS uint64_t*)(smem + L::kMasks);
+  const int i0 = rt * kRowsWg / p.H;  // first query row of the tile
+  int n_valid;
+  if constexpr (PR) {
+    const int n_i = (min((rt + 1) * kRowsWg, p.rows) - 1) / p.H - i0 + 1;
+    n_valid = compact_per_row(p, r, slot0, nslots, i0, n_i, smem, list, masks, tid);
+  } else {
+    n_valid = compact_slots<FP8>(p, r, slot0, nslots, smem, tid);
   }
 
   // ---- the first blocks' loads go out before the query rows, so that their
@@ -574,6 +674,14 @@ void partial_kernel(const PartialParams p) {
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) O[dt][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run[RG], l_run[RG];
+  // per-row selections: the bit of each of the lane's rows in the entry masks
+  // (rows past the end of the job are never stored; any bit will do)
+  int row_bit[RG];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
+    row_bit[rg] = PR ? min(max(row / p.H - i0, 0), 63) : 0;
+  }
 #pragma unroll
   for (int rg = 0; rg < RG; ++rg) {
     m_run[rg] = -INFINITY;
@@ -589,6 +697,14 @@ void partial_kernel(const PartialParams p) {
     // from LDS first: LDS reads complete in order).
     const int hn = h + L::kLead;
     const int b_next = hn < n_valid ? __builtin_amdgcn_readfirstlane(list[hn]) : -1;
+    uint64_t emask = ~0ull;  // the rows this entry is attended by
+    if constexpr (PR) {
+      // (readfirstlane returns int: widen through uint32_t, not by sign)
+      const uint64_t m = masks[h];
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32));
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)m);
+      emask = ((uint64_t)hi << 32) | (uint64_t)lo;
+    }
     __builtin_amdgcn_sched_barrier(0);
     // fp8: the scores are accumulated as ratio * (q_pe . kpe codes) +
     // q_lat . ckv codes (ratio = RoPE scale / latent scale) and then scaled by
@@ -801,6 +917,10 @@ void partial_kernel(const PartialParams p) {
         for (int k = 0; k < 4; ++k) bm = fmaxf(bm, acc[rg][tau][k]);
       }
       bmax[rg] = xor_max(bm);
+      if constexpr (PR) {
+        // a row that does not attend this entry: no maximum, no weights
+        if (((emask >> row_bit[rg]) & 1ull) == 0) bmax[rg] = -INFINITY;
+      }
       need_any |= bmax[rg] > m_run[rg] + kTau;
     }
     if (__ballot(need_any) != 0) {
@@ -826,9 +946,18 @@ void partial_kernel(const PartialParams p) {
     // need them, so that this VALU work runs beside the matrix core.
     bf16x8_t pb[RG][kKSteps];
     float psum[RG];
+    bool on[RG];
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg) on[rg] = !PR || ((emask >> row_bit[rg]) & 1ull) != 0;
     auto p_pair = [&](int rg, int tau, int k0) {
-      const float e0 = __builtin_amdgcn_exp2f(acc[rg][tau][k0] - m_run[rg]);
-      const float e1 = __builtin_amdgcn_exp2f(acc[rg][tau][k0 + 1] - m_run[rg]);
+      // (an exact 0 for rows that do not attend this entry, also before
+      // their first attended entry, when m_run is still -inf)
+      float e0 = __builtin_amdgcn_exp2f(acc[rg][tau][k0] - m_run[rg]);
+      float e1 = __builtin_amdgcn_exp2f(acc[rg][tau][k0 + 1] - m_run[rg]);
+      if constexpr (PR) {
+        e0 = on[rg] ? e0 : 0.f;
+        e1 = on[rg] ? e1 : 0.f;
+      }
       psum[rg] += e0 + e1;
       pb[rg][tau >> 1][(tau & 1) * 4 + k0] = (__bf16)(FP8 ? e0 * v_mult : e0);
       pb[rg][tau >> 1][(tau & 1) * 4 + k0 + 1] = (__bf16)(FP8 ? e1 * v_mult : e1);
@@ -929,18 +1058,22 @@ void partial_kernel(const PartialParams p) {
 
 }  // namespace
 
-template <int KV>
+template <int KV, bool PR = false>
 static void launch_kv(const PartialParams& p, int grid, int row_groups, hipStream_t s) {
   if (row_groups == 2)
-    hipLaunchKernelGGL((partial_kernel<2, KV>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_kernel<2, KV, PR>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((partial_kernel<1, KV>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_kernel<1, KV, PR>), dim3(grid), dim3(256), 0, s, p);
 }
 
-hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, hipStream_t s) {
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, bool per_row,
+                          hipStream_t s) {
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (kv == kKvFp8Shared)
+  if (per_row) {
+    if (kv != kKvBf16) return hipErrorInvalidValue;
+    launch_kv<kKvBf16, true>(p, grid, row_groups, s);
+  } else if (kv == kKvFp8Shared)
     launch_kv<kKvFp8Shared>(p, grid, row_groups, s);
   else if (kv == kKvFp8Split)
     launch_kv<kKvFp8Split>(p, grid, row_groups, s);

@@ -67,3 +67,40 @@ def test_packed_descriptor_equals_fieldwise():
              (torch.zeros(0, 4, dtype=torch.float32), None), (torch.zeros((), dtype=torch.float32), None)]
     for t, bs in cases:
         assert bytes(mla.describe(t, bs)) == bytes(_describe_fieldwise(t, bs)), (t.shape, t.stride())
+
+
+def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5):
+    """Call the partial entry point on CPU tensors: only the host-side checks
+    run (each of these calls must fail before anything is launched)."""
+    import types
+    import torch
+    from paper_2606_01502_amd import mla
+    kv = torch.uint8 if fp8 else torch.bfloat16
+    q_lat = torch.zeros((R, Mq, H, 512), dtype=torch.bfloat16)
+    q_pe = torch.zeros((R, Mq, H, 64), dtype=torch.bfloat16)
+    ckv = torch.zeros((P, 64, 512), dtype=kv)
+    kpe = torch.zeros((P, 64, 64), dtype=kv)
+    sc = torch.ones(P, dtype=torch.float32) if fp8 else None
+    table = torch.zeros((R, NB), dtype=torch.int32)
+    sel = torch.zeros(sel_shape, dtype=torch.int32)
+    stream = types.SimpleNamespace(cuda_stream=0)
+    try:
+        mla.sparse_partial_attn(q_lat, q_pe, ckv, kpe, table, sel, 0.1, ckv_scale=sc,
+                                kpe_scale=sc, stream=stream)
+    except mla.MlaError as e:
+        return e.status, str(e)
+    return mla.MLA_OK, ""
+
+
+def test_per_row_selection_host_checks():
+    from paper_2606_01502_amd import mla
+    st, msg = _cpu_call((2, 4, 3))  # Mq mismatch
+    assert st == mla.MLA_ERR_INVALID_ARGUMENT and "[R, Mq, K]" in msg
+    st, msg = _cpu_call((3, 3))  # R mismatch
+    assert st == mla.MLA_ERR_INVALID_ARGUMENT
+    st, msg = _cpu_call((2, 3, 3), fp8=True)
+    assert st == mla.MLA_ERR_UNSUPPORTED and "bf16" in msg
+    st, msg = _cpu_call((2, 3, 3), NB=40000)  # per-row counters would not fit in LDS
+    assert st == mla.MLA_ERR_UNSUPPORTED and "NB" in msg
+    st, msg = _cpu_call((2, 3, 3, 1))  # 4-d selection
+    assert st == mla.MLA_ERR_INVALID_ARGUMENT
