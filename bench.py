@@ -39,7 +39,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="batched-merge",
                     help="batched-merge | dsv3-one-request | few-head | dense-local | "
-                         "dense-local-fp8 | tiny")
+                         "dense-local-fp8 | tiny | holder-{dense|sparse}-n<N>-h<H>[-jobs] "
+                         "(one holder chunk serving N requesters)")
     ap.add_argument("--n-splits", type=int, default=0, help="split-K override (0 = library)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 = skip)")
@@ -172,15 +173,21 @@ def main():
         lse_np = out_lse.cpu().numpy()
         merged_np = merged.cpu().numpy() if merged is not None else None
 
+        # requesters are jobs (slot-major: hit j of every request, then hit
+        # j+1), or the query rows of one job (one holder serving them all)
+        rows_are_requests = R == 1 and n_req > 1 and Mq == n_req
+
         def jobs_of(reqs):
-            # slot-major like the workload: hit j of every sampled request, then hit j+1
             reqs = np.asarray(reqs)
-            return np.concatenate([j * n_req + reqs for j in range(parts)])
+            if rows_are_requests:
+                return (np.zeros(1, np.int64), reqs)
+            return (np.concatenate([j * n_req + reqs for j in range(parts)]), slice(None))
 
         def run_oracle(reqs):
-            js = jobs_of(reqs)
-            return js, oracle.partial(w.q_lat[js], w.q_pe[js], w.ckv, w.kpe, w.table[js], w.sel[js],
-                                      w.scale, w.ckv_scale, w.kpe_scale)
+            js, ri = jobs_of(reqs)
+            sel = w.sel[js][:, ri] if w.sel.ndim == 3 else w.sel[js]
+            return (js, ri), oracle.partial(w.q_lat[js][:, ri], w.q_pe[js][:, ri], w.ckv, w.kpe,
+                                            w.table[js], sel, w.scale, w.ckv_scale, w.kpe_scale)
 
         ts = time.perf_counter()
         js, (o1, l1) = run_oracle([0])
@@ -194,12 +201,13 @@ def main():
             pl = np.stack([l_ref[j * n:(j + 1) * n] for j in range(parts)])
             m_ref, _ = oracle.merge(po, pl)
         elapsed = time.perf_counter() - ts
+        js, ri = js
         cpu = {"value": elapsed * 1e6 / n, "unit": "us/request", "cores": oracle.default_threads(),
                "kind": "oracle",
                "sample": f"{n} of {n_req} requests ({len(js)} of {R} partial jobs"
                          f"{' + their merge' if parts > 1 else ''}), fp64 C oracle"}
-        rel = G.row_errors(out_np[js].astype(np.float64), o_ref)
-        lse_err = np.abs(lse_np[js] - l_ref)
+        rel = G.row_errors(out_np[js][:, ri].astype(np.float64), o_ref)
+        lse_err = np.abs(lse_np[js][:, ri] - l_ref)
         parity = {"rows": int(rel.size), "max_row_rel_err": float(rel.max()),
                   "max_lse_abs_err": float(lse_err[np.isfinite(l_ref)].max())
                   if np.isfinite(l_ref).any() else 0.0}

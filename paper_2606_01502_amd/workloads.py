@@ -168,10 +168,16 @@ class Workload:
         return self.ckv.dtype == np.uint8
 
     def n_selected_blocks(self):
+        """Blocks a job must read: its valid slots (one selection per job), or
+        the distinct blocks its query rows select (a selection per row)."""
+        if self.sel.ndim == 3:
+            return int(sum(np.unique(s[s >= 0]).size for s in self.sel))
         return int((self.sel >= 0).sum())
 
     def algorithmic_flops(self):
         R, Mq, H, _ = self.q_lat.shape
+        if self.sel.ndim == 3:  # each query row attends its own slots
+            return int((self.sel >= 0).sum()) * BLOCK * H * 2 * (DLAT + DPE + DLAT)
         per_job = (self.sel >= 0).sum(axis=1).astype(np.int64) * BLOCK
         return int((per_job * Mq * H).sum()) * 2 * (DLAT + DPE + DLAT)
 
@@ -299,6 +305,38 @@ def dense_local(seed=5, n_requests=32, chunk_blocks=1024, fp8=False):
     return w.to_fp8() if fp8 else w
 
 
+def holder(n_req, heads, sparse=False, as_jobs=False, seed=7):
+    """One holder chunk serving n_req routed requesters (Mq = 1, `heads`
+    heads each; q ~ N(0,1), cache ~ N(0,0.5)): the holder-compute experiment
+    of Section 6.3, on one GPU.
+      dense:  a 2048-token chunk (32 blocks), every requester attends all of
+              it (the paper's c_t = 2048 resident tokens);
+      sparse: an 8192-token chunk (128 blocks), each requester selects 32
+              blocks drawn Zipf(1.1) over positions, so hot blocks are shared.
+    By default the requesters are the query rows of one job (a shared
+    selection when dense, one selection per row when sparse) and the library
+    reads each block once for all of them; as_jobs routes every requester as
+    a job of its own on the same chunk (each reads its blocks itself)."""
+    nb = 128 if sparse else 32
+    q_lat, q_pe = _queries(seed, n_req, 1, heads)  # [n_req, 1, H, .]
+    ckv, kpe = _pool(seed, 2 * nb, 0.5)
+    perm = _perm(seed, 2 * nb)[:nb].astype(np.int32)  # the chunk's blocks, scattered in the pool
+    if sparse:
+        rs = np.random.default_rng([seed, _T_SEL])
+        rows = np.stack([zipf_ids(rs, nb, 32) for _ in range(n_req)]).astype(np.int32)
+    else:
+        rows = np.tile(np.arange(nb, dtype=np.int32), (n_req, 1))
+    name = f"holder-{'sparse' if sparse else 'dense'}-n{n_req}-h{heads}" + ("-jobs" if as_jobs else "")
+    if as_jobs:
+        return Workload(name, q_lat, q_pe, ckv, kpe, np.tile(perm, (n_req, 1)), rows,
+                        n_requests=n_req, merge_parts=1)
+    q_lat = np.ascontiguousarray(q_lat.reshape(1, n_req, heads, DLAT))
+    q_pe = np.ascontiguousarray(q_pe.reshape(1, n_req, heads, DPE))
+    sel = rows[:1] if not sparse else rows[None]
+    return Workload(name, q_lat, q_pe, ckv, kpe, perm[None], np.ascontiguousarray(sel),
+                    n_requests=n_req, merge_parts=1)
+
+
 CONFIGS = {
     "tiny": tiny,
     "dsv3-one-request": dsv3_one_request,
@@ -310,6 +348,13 @@ CONFIGS = {
 
 
 def make(name, seed=None, **kw):
+    """A named workload; `holder-{dense|sparse}-n{N}-h{H}[-jobs]` builds the
+    holder experiment (see holder)."""
+    if name.startswith("holder-"):
+        parts = name.split("-")
+        kw.update(n_req=int(parts[2][1:]), heads=int(parts[3][1:]),
+                  sparse=parts[1] == "sparse", as_jobs=parts[-1] == "jobs")
+        return holder(**kw) if seed is None else holder(seed=seed, **kw)
     fn = CONFIGS[name]
     return fn(**kw) if seed is None else fn(seed=seed, **kw)
 

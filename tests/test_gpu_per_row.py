@@ -99,3 +99,23 @@ def test_per_row_rejects_fp8_cache():
         mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"], t["sel"],
                                 w.scale, ckv_scale=t["ckv_scale"], kpe_scale=t["kpe_scale"])
     assert e.value.status == mla.MLA_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kind", ["dense", "sparse"])
+def test_holder_rows_match_jobs_and_oracle(kind):
+    """The holder workload served as one job whose query rows are the
+    requesters equals the same requesters routed as separate jobs, and both
+    match the oracle on sampled requesters."""
+    print(f"case: holder {kind} rows vs jobs", flush=True)
+    n, h = 24, 16
+    wr = W.make(f"holder-{kind}-n{n}-h{h}")
+    wj = W.make(f"holder-{kind}-n{n}-h{h}-jobs")
+    out_r, lse_r = G.run_partial(G.upload(wr), wr.scale)
+    out_j, lse_j = G.run_partial(G.upload(wj), wj.scale)
+    G.assert_parity(out_r.reshape(out_j.shape), lse_r.reshape(lse_j.shape), out_j, lse_j,
+                    f"holder {kind} rows vs jobs")
+    req = np.array([0, 5, 11, 23])
+    ref_o, ref_l = oracle.partial(wj.q_lat[req], wj.q_pe[req], wj.ckv, wj.kpe, wj.table[req],
+                                  wj.sel[req], wj.scale)
+    G.assert_parity(out_r[0, req][:, None], lse_r[0, req][:, None], ref_o, ref_l,
+                    f"holder {kind} vs oracle")
