@@ -132,8 +132,16 @@ mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor
 /* Tuning and test controls for mla_sparse_partial_attn_ex.  Zero fields mean
  * "library's choice"; the result is the same up to rounding for any value. */
 typedef struct {
-  int32_t n_splits;    /* split-K: slot ranges per job, 1..K (0 = automatic) */
-  int32_t reserved[7]; /* must be zero                                        */
+  /* split-K: work splits per job (0 = automatic).  A shared selection, or
+   * per-row selections whose K slots times the query rows of a row tile
+   * exceed 1024, split into ranges of slots (1..K); other per-row selections
+   * split by logical block, split s taking blocks s, s + n, s + 2n, ...
+   * (1..NB). */
+  int32_t n_splits;
+  /* rows per work item: 64 or 128 (0 = automatic: 128 when Mq * H > 64 and
+   * the splits are long, else 64). */
+  int32_t row_tile;
+  int32_t reserved[6]; /* must be zero */
 } mla_partial_opts_t;
 
 /* mla_sparse_partial_attn with explicit options (opts may be NULL). */

@@ -170,9 +170,11 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if ((st = check_tensor(out_lat, "out_lat", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
     if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
     if (opts) {
-      for (int i = 0; i < 7; ++i)
+      for (int i = 0; i < 6; ++i)
         if (opts->reserved[i]) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.reserved must be zero");
       if (opts->n_splits < 0) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.n_splits must be >= 0");
+      if (opts->row_tile != 0 && opts->row_tile != 64 && opts->row_tile != 128)
+        return fail(MLA_ERR_INVALID_ARGUMENT, "opts.row_tile must be 0, 64 or 128");
     }
 
     const int64_t R = q_lat->shape[0], Mq = q_lat->shape[1], H = q_lat->shape[2];
@@ -226,6 +228,19 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     // ---- plan: row tiles of 128 or 64 rows (4 waves of 32 or 16 rows);
     // split-K over slot ranges so that the grid covers the chip
     int row_groups = rows > 64 ? 2 : 1;
+    if (opts && opts->row_tile) {
+      row_groups = opts->row_tile / 64;
+    } else if (row_groups == 2) {
+      // 128-row tiles read each block once for twice the rows, which pays
+      // when splits are long; when the grid covers the chip only with short
+      // splits (under 8 blocks each), 64-row tiles finish sooner: twice the
+      // work items, each with half the fixed cost (query rows in, partial
+      // rows out)
+      const int64_t units2 = R * ((rows + 127) / 128);
+      const int64_t s2 = std::min<int64_t>((device_cus() + units2 - 1) / units2,
+                                           std::max<int64_t>(K / 2, 1));
+      if (K < 8 * s2) row_groups = 1;
+    }
     // per-row selections: the query rows a row tile spans (one mask bit each)
     auto tile_query_rows = [&](int rg) {
       const int64_t rw = 64 * rg;
@@ -238,7 +253,11 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     };
     int64_t tile_qrows = 1;
     if (per_row) {
-      if (row_groups == 2 && tile_query_rows(2) > mla::kPerRowMaxRows) row_groups = 1;
+      if (row_groups == 2 && tile_query_rows(2) > mla::kPerRowMaxRows) {
+        if (opts && opts->row_tile == 128)
+          return fail(MLA_ERR_UNSUPPORTED, "per-row selections: too many query rows per 128-row tile");
+        row_groups = 1;
+      }
       tile_qrows = tile_query_rows(row_groups);
       if (tile_qrows > mla::kPerRowMaxRows)
         return fail(MLA_ERR_UNSUPPORTED, "per-row selections: too many query rows per tile");
@@ -247,9 +266,17 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     }
     const int rows_wg = 64 * row_groups;
     const int64_t row_tiles = (rows + rows_wg - 1) / rows_wg;
+    // per-row selections whose tile slots all fit one list split by logical
+    // block: every split then scans all slots and the rows that chose a block
+    // in different slots still share its load
+    const bool by_id = per_row && tile_qrows > 1 && K * tile_qrows <= mla::kMaxSlotsPerSplit;
     int64_t S;
     if (opts && opts->n_splits > 0) {
-      S = std::min<int64_t>(opts->n_splits, std::max<int64_t>(K, 1));
+      S = std::min<int64_t>(opts->n_splits, std::max<int64_t>(by_id ? NB : K, 1));
+    } else if (by_id) {
+      const int64_t units = R * row_tiles;
+      S = std::max<int64_t>(1, (device_cus() + units - 1) / units);
+      S = std::min<int64_t>(S, std::max<int64_t>(std::min<int64_t>(NB, K * tile_qrows) / 2, 1));
     } else {
       // enough work items to cover the chip, but at least two slots per split:
       // a split of one block costs more in fixed latency (its prologue,
@@ -260,10 +287,13 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     }
     // a split's block list holds at most kMaxSlotsPerSplit entries: its slots,
     // or for per-row selections its slots of every query row of the tile
-    S = std::max<int64_t>(S, (K * tile_qrows + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
-    int64_t sps = std::max<int64_t>(1, (K + S - 1) / S);
-    if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, mla::kMaxSlotsPerSplit / tile_qrows));
-    S = std::max<int64_t>(1, (K + sps - 1) / sps);
+    int64_t sps = K;
+    if (!by_id) {
+      S = std::max<int64_t>(S, (K * tile_qrows + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
+      sps = std::max<int64_t>(1, (K + S - 1) / S);
+      if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, mla::kMaxSlotsPerSplit / tile_qrows));
+      S = std::max<int64_t>(1, (K + sps - 1) / sps);
+    }
     if (R * row_tiles * S > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "grid too large");
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -289,6 +319,7 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     p.rows = (int32_t)rows;
     p.n_splits = (int32_t)S;
     p.slots_per_split = (int32_t)sps;
+    p.split_by_id = by_id ? 1 : 0;
     p.row_tiles = (int32_t)row_tiles;
     p.scale_log2 = (float)((double)scale * 1.4426950408889634074);
     p.out = (float*)out_lat->data;

@@ -33,6 +33,9 @@ struct PartialParams {
   int32_t NB, K;
   int32_t Mq, H, rows;  // rows = Mq * H
   int32_t n_splits, slots_per_split, row_tiles;
+  // per-row selections split by logical block instead of by slot range: split
+  // s takes blocks s, s + n_splits, ... from all K slots of every row
+  int32_t split_by_id;
   float scale_log2;  // softmax scale * log2(e)
   // destination: direct (n_splits == 1) or split-K workspace
   float* out;

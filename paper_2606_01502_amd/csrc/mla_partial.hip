@@ -521,44 +521,48 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
 }
 
 // Per-row selections: compact the blocks that query rows i0 .. i0 + n_i - 1
-// of job r select in slots [slot0, slot0 + nslots) into the LDS list, each
+// of job r select in slots [slot0, slot0 + nslots), among the logical blocks
+// id0, id0 + id_step, id0 + 2 id_step, ... below NB, into the LDS list, each
 // block once per copy, with a mask of the rows that hold that copy: a block
 // that row i lists c_i times gives max_i c_i entries, entry k carrying the
 // rows with c_i > k.  Each row thus attends exactly its own multiset, and a
 // block that several rows chose is loaded once for all of them.  Entries
 // come in ascending logical-block order.  The counters (16 bits per (block,
-// row); at most nslots each) use the stage area, which is free until the
-// first load is issued.  Returns the number of entries.
+// row) of the blocks taken; at most nslots each) use the stage area, which is
+// free until the first load is issued.  Returns the number of entries.
 __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, int slot0,
-                                               int nslots, int i0, int n_i, LDS uint8_t* smem,
-                                               LDS int* list, LDS uint64_t* masks, int tid) {
+                                               int nslots, int id0, int id_step, int i0, int n_i,
+                                               LDS uint8_t* smem, LDS int* list,
+                                               LDS uint64_t* masks, int tid) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   LDS uint32_t* cnt = (LDS uint32_t*)smem;
   LDS const uint16_t* cnt16 = (LDS const uint16_t*)smem;
   LDS int* wave_cnt = (LDS int*)(smem + Layout<false>::kWaveCnt);
-  const int n_words = (p.NB * n_i + 1) >> 1;
+  const int n_ids = id0 < p.NB ? (p.NB - id0 + id_step - 1) / id_step : 0;
+  const int n_words = (n_ids * n_i + 1) >> 1;
   for (int w = tid; w < n_words; w += 256) cnt[w] = 0u;
   lds_barrier();
   const int n_ent = n_i * nslots;
   for (int e = tid; e < n_ent; e += 256) {
     const int ii = e / nslots, j = e - ii * nslots;
     const int id = p.sel[r * p.sel_s0 + (int64_t)(i0 + ii) * p.sel_s1 + slot0 + j];
-    if (id >= 0 && id < p.NB) {
+    const int u = (id - id0) / id_step;
+    if (id >= id0 && id < p.NB && u * id_step == id - id0) {
       const int bb = p.table[r * p.table_s0 + id];
       if (bb >= 0 && bb < p.P) {
-        const int c = id * n_i + ii;
+        const int c = u * n_i + ii;
         __atomic_fetch_add(&cnt[c >> 1], 1u << ((c & 1) * 16), __ATOMIC_RELAXED);
       }
     }
   }
   lds_barrier();
   int n_valid = 0;
-  for (int base = 0; base < p.NB; base += 256) {
-    const int id = base + tid;
+  for (int base = 0; base < n_ids; base += 256) {
+    const int u = base + tid, id = id0 + u * id_step;
     int kmax = 0;
-    if (id < p.NB)
-      for (int ii = 0; ii < n_i; ++ii) kmax = max(kmax, (int)cnt16[id * n_i + ii]);
+    if (u < n_ids)
+      for (int ii = 0; ii < n_i; ++ii) kmax = max(kmax, (int)cnt16[u * n_i + ii]);
     // exclusive prefix sum of kmax over the workgroup (ascending id)
     int incl = kmax;
 #pragma unroll
@@ -580,7 +584,7 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
       for (int k = 0; k < kmax; ++k) {
         uint64_t m = 0;
         for (int ii = 0; ii < n_i; ++ii)
-          if ((int)cnt16[id * n_i + ii] > k) m |= 1ull << ii;
+          if ((int)cnt16[u * n_i + ii] > k) m |= 1ull << ii;
         list[off + k] = bb;
         masks[off + k] = m;
       }
@@ -632,7 +636,12 @@ void partial_kernel(const PartialParams p) {
   int n_valid;
   if constexpr (PR) {
     const int n_i = (min((rt + 1) * kRowsWg, p.rows) - 1) / p.H - i0 + 1;
-    n_valid = compact_per_row(p, r, slot0, nslots, i0, n_i, smem, list, masks, tid);
+    // split by logical block (split s takes blocks s, s + S, ... from every
+    // slot), so that rows which chose one block in different slots share its
+    // load; or by slot range when a tile's slots may not fit one list
+    n_valid = p.split_by_id
+                  ? compact_per_row(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
+                  : compact_per_row(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
   } else {
     n_valid = compact_slots<FP8>(p, r, slot0, nslots, smem, tid);
   }
@@ -827,7 +836,10 @@ void partial_kernel(const PartialParams p) {
               st_pair<true, false, true>(c0, c1, a[t0], a[t0 + 1], q);
             else if ((step == 17 || (kSplitScales && step == 1)) && last)
               st_pair<false, true, false>(c0, c1, a[t0], a[t0 + 1], q);
-            else if (kSplitScales && step == 2 && j == 0)
+            else if (kSplitScales && step == 2)
+              // every pair leads with the wait states: the ratio's VALU
+              // writes, and any register copies the compiler places after
+              // them, may end right before it
               st_pair<false, false, true>(c0, c1, a[t0], a[t0 + 1], q);
             else
               st_pair<false, false, false>(c0, c1, a[t0], a[t0 + 1], q);

@@ -42,7 +42,8 @@ class Tensor(ctypes.Structure):
 
 
 class PartialOpts(ctypes.Structure):
-    _fields_ = [("n_splits", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+    _fields_ = [("n_splits", ctypes.c_int32), ("row_tile", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 6)]
 
 
 _lib = None
@@ -143,7 +144,7 @@ class _Prepared:
 
 
 def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
-                  out_lat, out_lse, ckv_scale, kpe_scale, n_splits, stream):
+                  out_lat, out_lse, ckv_scale, kpe_scale, n_splits, row_tile, stream):
     R, Mq, H, _ = q_lat.shape
     if out_lat is None:
         out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
@@ -151,6 +152,7 @@ def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_
         out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
     opts = PartialOpts()
     opts.n_splits = int(n_splits)
+    opts.row_tile = int(row_tile)
     descs = (describe(q_lat), describe(q_pe), describe(ckv_pool, ckv_scale),
              describe(kpe_pool, kpe_scale), describe(chunk_block_table), describe(sel_block_ids))
     outs = (describe(out_lat), describe(out_lse))
@@ -163,19 +165,19 @@ def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_
 
 def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                     out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None, n_splits=0,
-                    stream=None):
+                    row_tile=0, stream=None):
     """sparse_partial_attn with every argument fixed, the stream included
     (the current one when None); calling the result launches the work and
     returns (out_lat, out_lse)."""
     args, keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                        sel_block_ids, scale, out_lat, out_lse, ckv_scale,
-                                       kpe_scale, n_splits, stream)
+                                       kpe_scale, n_splits, row_tile, stream)
     return _Prepared(load().mla_sparse_partial_attn_ex, args, keep, result)
 
 
 def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
                         scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
-                        n_splits=0, stream=None):
+                        n_splits=0, row_tile=0, stream=None):
     """Partial attention of each job's Mq x H rows over its selected blocks.
 
     Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
@@ -183,7 +185,7 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     lib = load()
     args, _keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                         sel_block_ids, scale, out_lat, out_lse, ckv_scale,
-                                        kpe_scale, n_splits, stream)
+                                        kpe_scale, n_splits, row_tile, stream)
     _check(lib, lib.mla_sparse_partial_attn_ex(*args))
     return result
 

@@ -17,9 +17,9 @@ from tests import gpu_helpers as G
 pytestmark = pytest.mark.gpu
 
 
-def _check(w, n_splits=0, what="", jobs=None):
+def _check(w, n_splits=0, what="", jobs=None, row_tile=0):
     t = G.upload(w)
-    out, lse = G.run_partial(t, w.scale, n_splits=n_splits)
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits, row_tile=row_tile)
     if jobs is None:
         ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
                                       w.ckv_scale, w.kpe_scale)
@@ -36,15 +36,18 @@ def _check(w, n_splits=0, what="", jobs=None):
 def test_fp8_random_splits(n_splits, shared):
     print(f"case: fp8 random splits={n_splits} shared={shared}", flush=True)
     w = W.random_case(201, R=3, Mq=1, H=128, P=20, NB=9, K=7, sigma=0.5).to_fp8(shared)
-    _check(w, n_splits)
+    for rt in (64, 128):
+        _check(w, n_splits, f"fp8 splits={n_splits} row_tile={rt}", row_tile=rt)
 
 
 @pytest.mark.parametrize("mq,h", [(1, 1), (1, 16), (2, 40), (1, 64), (3, 64), (2, 128), (5, 31)])
 def test_fp8_ragged_rows(mq, h):
     print(f"case: fp8 ragged mq={mq} h={h}", flush=True)
     w = W.random_case(202 + 1000 * mq + h, R=2, Mq=mq, H=h, P=12, NB=6, K=3, sigma=0.7)
-    _check(w.to_fp8(), 0, f"ragged {mq}x{h} shared")
-    _check(w.to_fp8(shared_scale=False), 0, f"ragged {mq}x{h} separate")
+    for rt in (64, 128):
+        _check(w.to_fp8(), 0, f"ragged {mq}x{h} shared row_tile={rt}", row_tile=rt)
+        _check(w.to_fp8(shared_scale=False), 0, f"ragged {mq}x{h} separate row_tile={rt}",
+               row_tile=rt)
 
 
 @pytest.mark.parametrize("shared", [True, False])

@@ -24,9 +24,9 @@ def _oracle(w, jobs=None):
                           w.scale, w.ckv_scale, w.kpe_scale)
 
 
-def _check_case(w, n_splits=0, what=""):
+def _check_case(w, n_splits=0, what="", row_tile=0):
     t = G.upload(w)
-    out, lse = G.run_partial(t, w.scale, n_splits=n_splits)
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits, row_tile=row_tile)
     ref_o, ref_l = _oracle(w)
     return G.assert_parity(out, lse, ref_o, ref_l, what or w.name)
 
@@ -43,20 +43,23 @@ def test_small_random_all_splits(n_splits):
     _check_case(w, n_splits)
 
 
+@pytest.mark.parametrize("row_tile", [0, 64, 128])
 @pytest.mark.parametrize("mq,h", [(1, 1), (3, 7), (1, 64), (2, 40), (1, 128), (2, 128), (5, 31)])
-def test_ragged_rows(mq, h):
-    """Row counts below, at and above the 64- and 128-row tiles."""
-    print(f"case: ragged mq={mq} h={h}", flush=True)
+def test_ragged_rows(mq, h, row_tile):
+    """Row counts below, at and above the 64- and 128-row tiles, with the
+    library's tile choice and each tile size forced."""
+    print(f"case: ragged mq={mq} h={h} row_tile={row_tile}", flush=True)
     w = W.random_case(102 + mq * 1000 + h, R=2, Mq=mq, H=h, P=12, NB=6, K=3, sigma=0.7)
-    _check_case(w)
+    _check_case(w, row_tile=row_tile)
 
 
 def test_padding_duplicates_and_empty_jobs():
     print("case: padding", flush=True)
-    w = W.random_case(103, R=4, Mq=1, H=32, P=10, NB=6, K=6, n_valid=[0, 1, 3, 6],
+    w = W.random_case(103, R=4, Mq=3, H=32, P=10, NB=6, K=6, n_valid=[0, 1, 3, 6],
                       allow_dup=True, pad_pattern="interleaved")
     for s in (0, 1, 2, 6):
-        _check_case(w, s, f"padding splits={s}")
+        for rt in (64, 128):
+            _check_case(w, s, f"padding splits={s} row_tile={rt}", row_tile=rt)
 
 
 def test_no_slots_at_all():
@@ -117,7 +120,8 @@ def test_split_invariance_gpu_only():
     print("case: split invariance", flush=True)
     w = W.random_case(109, R=2, Mq=1, H=128, P=40, NB=33, K=32, sigma=0.5)
     t = G.upload(w)
-    outs = [G.run_partial(t, w.scale, n_splits=s) for s in (1, 2, 4, 32)]
+    outs = [G.run_partial(t, w.scale, n_splits=s, row_tile=rt) for rt in (128, 64)
+            for s in (1, 2, 4, 32)]
     for o, l in outs[1:]:
         assert np.abs(l - outs[0][1]).max() < 1e-4
         assert G.row_errors(o, outs[0][0]).max() < 5e-3

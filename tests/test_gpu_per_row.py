@@ -14,23 +14,30 @@ from tests import gpu_helpers as G
 pytestmark = pytest.mark.gpu
 
 
-def _check(w, n_splits=0, what=""):
+def _check(w, n_splits=0, what="", row_tile=0):
     t = G.upload(w)
-    out, lse = G.run_partial(t, w.scale, n_splits=n_splits)
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits, row_tile=row_tile)
     ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale)
     return G.assert_parity(out, lse, ref_o, ref_l, what or w.name)
 
 
 @pytest.mark.parametrize("mq,h", [(4, 16), (8, 16), (3, 40), (2, 128), (64, 2), (70, 1),
                                   (5, 31), (1, 64)])
-def test_per_row_layouts(mq, h):
+@pytest.mark.parametrize("row_tile", [0, 64, 128])
+def test_per_row_layouts(mq, h, row_tile):
     """Row tiles of 128 rows spanning 8 query rows, tiles straddling query
     rows (H = 40, 31), one query row per tile (H = 128), 64 query rows per
-    tile (H = 2), and H = 1, where the library falls back to 64-row tiles."""
-    print(f"case: per-row mq={mq} h={h}", flush=True)
+    tile (H = 2), and H = 1, where a 128-row tile would span more query rows
+    than a mask holds (the library takes 64-row tiles; forcing 128 fails)."""
+    print(f"case: per-row mq={mq} h={h} row_tile={row_tile}", flush=True)
     w = W.random_case(600 + 100 * mq + h, R=2, Mq=mq, H=h, P=30, NB=12, K=6, sigma=0.7,
                       per_row=True, shared_frac=0.6)
-    _check(w, 0, f"per-row {mq}x{h}")
+    if h == 1 and mq > 64 and row_tile == 128:
+        with pytest.raises(mla.MlaError) as e:
+            _check(w, 0, row_tile=row_tile)
+        assert e.value.status == mla.MLA_ERR_UNSUPPORTED
+        return
+    _check(w, 0, f"per-row {mq}x{h} row_tile={row_tile}", row_tile=row_tile)
 
 
 @pytest.mark.parametrize("n_splits", [1, 2, 3, 7])
@@ -43,7 +50,20 @@ def test_per_row_splits_duplicates_padding(n_splits):
                       n_valid=n_valid, allow_dup=True, pad_pattern="interleaved",
                       per_row=True, shared_frac=0.5)
     assert (w.sel[0, 1] == -1).all()
-    _check(w, n_splits, f"per-row dup splits={n_splits}")
+    for rt in (64, 128):
+        _check(w, n_splits, f"per-row dup splits={n_splits} row_tile={rt}", row_tile=rt)
+
+
+@pytest.mark.parametrize("n_splits", [0, 1, 5])
+def test_per_row_long_selections_split_by_slot(n_splits):
+    """Four query rows per 128-row tile selecting 300 blocks each: the tile's
+    slots overflow one block list, so splits take slot ranges (the short
+    selections above split by logical block instead); ids repeat across and
+    within rows."""
+    print(f"case: per-row long selections splits={n_splits}", flush=True)
+    w = W.random_case(655 + n_splits, R=1, Mq=4, H=32, P=500, NB=400, K=300, sigma=0.5,
+                      allow_dup=True, per_row=True, shared_frac=0.5)
+    _check(w, n_splits, f"per-row K=300 splits={n_splits}")
 
 
 def test_per_row_invalid_ids_are_skipped():
