@@ -38,7 +38,7 @@ def _load(path=None):
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     lib.oracle_partial.restype = i32
     lib.oracle_partial.argtypes = [i32, i32, i32, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp,
-                                   vp, vp, i32, dbl, vp, vp, i32]
+                                   vp, vp, i32, i32, dbl, vp, vp, i32]
     lib.oracle_merge.restype = i32
     lib.oracle_merge.argtypes = [i32, i64, i32, vp, vp, vp, vp, i32]
     lib.oracle_bf16_to_f64.restype = dbl
@@ -70,14 +70,16 @@ def e4m3fn_to_f64(code):
 
 
 def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=None,
-            n_threads=None, lib=None):
+            n_threads=None, lib=None, tokens=False):
     """Oracle partial attention.
 
     q_lat uint16 [R, Mq, H, 512] and q_pe uint16 [R, Mq, H, 64] hold bf16 bits;
     ckv [P, 64, 512] / kpe [P, 64, 64] hold bf16 bits (uint16) or e4m3fn codes
     (uint8, with float32 per-block scales ckv_scale / kpe_scale [P]);
     table int32 [R, NB]; sel int32 [R, K] (one selection per job) or
-    [R, Mq, K] (one per query row); -1 = empty slot.
+    [R, Mq, K] (one per query row); -1 = empty slot.  A slot names a logical
+    block (all 64 tokens), or with tokens=True one logical token s (token
+    s % 64 of logical block s // 64).
     Returns (out float64 [R, Mq, H, 512], lse float64 [R, Mq, H]).
     """
     lib = lib or _load()
@@ -107,7 +109,7 @@ def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=
     lse = np.zeros((R, Mq, H), np.float64)
     rc = lib.oracle_partial(R, Mq, H, P, NB, K, _ptr(q_lat), _ptr(q_pe), kind, _ptr(ckv),
                             _ptr(kpe), _ptr(cs), _ptr(ks), _ptr(table), _ptr(sel),
-                            int(per_row), float(scale), _ptr(out), _ptr(lse),
+                            int(per_row), int(bool(tokens)), float(scale), _ptr(out), _ptr(lse),
                             int(n_threads or default_threads()))
     if rc != 0:
         raise ValueError("oracle_partial: invalid selected id or table entry")

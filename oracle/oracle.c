@@ -21,7 +21,9 @@
  *     requester, and Section 3.3: a selected cache entry keeps the position
  *     it was cached at.  So the holder applies no mask and no rotation.
  *   - Section 3.3 and Section 6.3: the selection-regime holder attends only
- *     the indexer's selected entries; here selection is by 64-token blocks.
+ *     the indexer's selected entries: here either 64-token blocks, or single
+ *     tokens (an indexer's top-k tokens, the selection budgets that Section
+ *     6.3 sweeps).
  *   - Section 2.2 and Section 3.3: partials are recombined by online softmax;
  *     the merge is commutative and has a zero-weight identity.
  *
@@ -102,10 +104,13 @@ static double kpe_at(const kv_view* kv, int64_t b, int t, int d) {
  *                  [R][K], one selection for all rows of a job; 1:
  *                  [R][Mq][K], a selection per query row (one holder serving
  *                  several routed requesters on one chunk, Section 6.3)
+ *   sel_tokens     0: a slot names a logical block, all 64 of its tokens;
+ *                  1: a slot names one logical token s of the chunk, token
+ *                  s % 64 of logical block s / 64
  *   out   [R][Mq][H][512], lse [R][Mq][H]        double, written
  *
- * For job r and row (i, h), with T the multiset of tokens (b, t) of the
- * blocks selected for the row (by the job, or by query row i):
+ * For job r and row (i, h), with T the multiset of tokens (b, t) selected
+ * for the row (by the job, or by query row i):
  *   s(b,t) = scale * (q_lat . ckv[b][t] + q_pe . kpe[b][t])
  *   lse    = ln sum_T exp(s)                    (via its maximum M)
  *   out    = sum_T exp(s - lse) * ckv[b][t]
@@ -118,7 +123,8 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
                    const uint16_t* q_lat, const uint16_t* q_pe, int kv_kind,
                    const void* ckv, const void* kpe, const float* ckv_scale,
                    const float* kpe_scale, const int32_t* table, const int32_t* sel,
-                   int sel_per_row, double scale, double* out, double* lse, int n_threads) {
+                   int sel_per_row, int sel_tokens, double scale, double* out, double* lse,
+                   int n_threads) {
   kv_view kv = {kv_kind, ckv, kpe, ckv_scale, kpe_scale};
   int bad = 0;
   if (kv_kind != ORACLE_KV_BF16 && kv_kind != ORACLE_KV_E4M3FN) return -1;
@@ -128,14 +134,17 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
   const int64_t sel_s1 = sel_per_row ? K : 0;
   const int64_t sel_s0 = sel_per_row ? (int64_t)Mq * K : K;
   const int n_sel = sel_per_row ? Mq : 1;
+  /* A slot covers `per_slot` tokens; logical ids run below NB * per_slot. */
+  const int per_slot = sel_tokens ? 1 : ORACLE_BLOCK;
+  const int64_t n_ids = sel_tokens ? (int64_t)NB * ORACLE_BLOCK : NB;
 
   /* Check every selected id and table entry before computing anything. */
   for (int r = 0; r < R; ++r)
     for (int64_t jj = 0; jj < (int64_t)n_sel * K; ++jj) {
       int32_t s = sel[(int64_t)r * sel_s0 + jj];
       if (s == -1) continue;
-      if (s < 0 || s >= NB) return -1;
-      int32_t b = table[(int64_t)r * NB + s];
+      if (s < 0 || s >= n_ids) return -1;
+      int32_t b = table[(int64_t)r * NB + (sel_tokens ? s / ORACLE_BLOCK : s)];
       if (b < 0 || (int64_t)b >= P) return -1;
     }
 
@@ -152,7 +161,7 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
     /* The token multiset of this row, in slot order. */
     int n_tok = 0;
     for (int j = 0; j < K; ++j)
-      if (row_sel[j] != -1) n_tok += ORACLE_BLOCK;
+      if (row_sel[j] != -1) n_tok += per_slot;
     for (int d = 0; d < ORACLE_DLAT; ++d) o[d] = 0.0;
     if (n_tok == 0) {
       lse[row] = -INFINITY;
@@ -172,8 +181,9 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
     for (int j = 0; j < K; ++j) {
       int32_t s = row_sel[j];
       if (s == -1) continue;
-      int64_t b = table[(int64_t)r * NB + s];
-      for (int t = 0; t < ORACLE_BLOCK; ++t) {
+      int64_t b = table[(int64_t)r * NB + (sel_tokens ? s / ORACLE_BLOCK : s)];
+      int t0 = sel_tokens ? s % ORACLE_BLOCK : 0;
+      for (int t = t0; t < t0 + per_slot; ++t) {
         double dot = 0.0;
         for (int d = 0; d < ORACLE_DLAT; ++d)
           dot += oracle_bf16_to_f64(ql[d]) * ckv_at(&kv, b, t, d);

@@ -149,13 +149,14 @@ class Workload:
     ckv: np.ndarray              # uint16 [P, 64, 512] (or uint8 codes)
     kpe: np.ndarray              # uint16 [P, 64, 64]  (or uint8 codes)
     table: np.ndarray            # int32  [R, NB]
-    sel: np.ndarray              # int32  [R, K]
+    sel: np.ndarray              # int32  [R, K] (or [R, Mq, K])
     scale: float = SCALE
     ckv_scale: np.ndarray | None = None  # float32 [P] for fp8 pools
     kpe_scale: np.ndarray | None = None
     n_requests: int = 0          # routed requests the call serves
     merge_parts: int = 1         # partials merged per request (slot-major jobs)
     meta: dict = field(default_factory=dict)
+    tokens: bool = False         # sel holds logical token ids (block * 64 + t)
 
     @property
     def shape(self):
@@ -169,21 +170,25 @@ class Workload:
 
     def n_selected_blocks(self):
         """Blocks a job must read: its valid slots (one selection per job), or
-        the distinct blocks its query rows select (a selection per row)."""
+        the distinct blocks its query rows select (a selection per row).  For
+        token selections: the valid slots / 64 (a token is 1/64 of a block)."""
+        if self.tokens:
+            return (self.sel >= 0).sum() / BLOCK
         if self.sel.ndim == 3:
             return int(sum(np.unique(s[s >= 0]).size for s in self.sel))
         return int((self.sel >= 0).sum())
 
     def algorithmic_flops(self):
         R, Mq, H, _ = self.q_lat.shape
+        per_slot = 1 if self.tokens else BLOCK
         if self.sel.ndim == 3:  # each query row attends its own slots
-            return int((self.sel >= 0).sum()) * BLOCK * H * 2 * (DLAT + DPE + DLAT)
-        per_job = (self.sel >= 0).sum(axis=1).astype(np.int64) * BLOCK
+            return int((self.sel >= 0).sum()) * per_slot * H * 2 * (DLAT + DPE + DLAT)
+        per_job = (self.sel >= 0).sum(axis=1).astype(np.int64) * per_slot
         return int((per_job * Mq * H).sum()) * 2 * (DLAT + DPE + DLAT)
 
     def kv_bytes(self):
         per_tok = (DLAT + DPE) * (1 if self.fp8 else 2)
-        b = self.n_selected_blocks() * BLOCK * per_tok
+        b = int(round(self.n_selected_blocks() * BLOCK * per_tok))
         if self.fp8:
             b += self.n_selected_blocks() * 8  # two fp32 scales per block
         return b
@@ -201,7 +206,7 @@ class Workload:
             kpe, ks = quantize_blocks_e4m3fn(self.kpe)
         return Workload(self.name + "-fp8", self.q_lat, self.q_pe, ckv, kpe, self.table,
                         self.sel, self.scale, cs, ks, self.n_requests, self.merge_parts,
-                        dict(self.meta))
+                        dict(self.meta), self.tokens)
 
 
 def _perm(seed, n):
@@ -385,18 +390,20 @@ def _slot_ids(rs, NB, K, nv, allow_dup, pad_pattern, common=None, shared_frac=0.
 
 
 def random_case(seed, R, Mq, H, P, NB, K, n_valid=None, sigma=1.0, allow_dup=False,
-                pad_pattern="tail", per_row=False, shared_frac=0.5):
+                pad_pattern="tail", per_row=False, shared_frac=0.5, tokens=False):
     """Small random case for tests: R jobs over a P-block pool, NB logical
     blocks per job, K slots of which n_valid[r] hold ids.  pad_pattern is
     'tail' (ids first), 'interleaved' (empty slots spread) or 'none'.
     per_row gives every query row its own selection, sel [R, Mq, K], drawing
     each id from a per-job common set with probability shared_frac so that
-    rows overlap; n_valid may then be [R][Mq]."""
+    rows overlap; n_valid may then be [R][Mq].  tokens draws logical token
+    ids in [0, 64 NB) instead of block ids."""
     q_lat, q_pe = _queries(seed, R, Mq, H, sigma)
     ckv, kpe = _pool(seed, P, sigma)
     rng = np.random.default_rng([seed, _T_TABLE])
     table = np.stack([rng.choice(P, NB, replace=NB > P) for _ in range(R)]).astype(np.int32)
     rs = np.random.default_rng([seed, _T_SEL])
+    n_ids = NB * BLOCK if tokens else NB
 
     def nvalid(r, i=None):
         if n_valid is None:
@@ -407,13 +414,13 @@ def random_case(seed, R, Mq, H, P, NB, K, n_valid=None, sigma=1.0, allow_dup=Fal
     if per_row:
         sel = np.full((R, Mq, K), -1, np.int32)
         for r in range(R):
-            common = rs.choice(NB, min(NB, K), replace=False)
+            common = rs.choice(n_ids, min(n_ids, K), replace=False)
             for i in range(Mq):
-                sel[r, i] = _slot_ids(rs, NB, K, nvalid(r, i), allow_dup, pad_pattern, common,
-                                      shared_frac)
+                sel[r, i] = _slot_ids(rs, n_ids, K, nvalid(r, i), allow_dup, pad_pattern,
+                                      common, shared_frac)
     else:
         sel = np.full((R, K), -1, np.int32)
         for r in range(R):
-            sel[r] = _slot_ids(rs, NB, K, nvalid(r), allow_dup, pad_pattern)
+            sel[r] = _slot_ids(rs, n_ids, K, nvalid(r), allow_dup, pad_pattern)
     return Workload(f"random-{seed}", q_lat, q_pe, ckv, kpe, table, sel,
-                    n_requests=R, merge_parts=1)
+                    n_requests=R, merge_parts=1, tokens=tokens)

@@ -73,6 +73,9 @@ def brute_force(w, rows=None):
         for s in (w.sel[r, i] if w.sel.ndim == 3 else w.sel[r]):
             if s < 0:
                 continue
+            if w.tokens:  # one logical token: token s % 64 of logical block s // 64
+                toks.append((int(w.table[r, s // BLOCK]), int(s % BLOCK)))
+                continue
             b = int(w.table[r, s])
             toks.extend((b, t) for t in range(BLOCK))
         if not toks:
@@ -167,6 +170,67 @@ def pin_per_row_is_one_job_per_row(lib):
     sel = w.sel.reshape(R * Mq, -1)
     o2, l2 = oracle.partial(q_lat, q_pe, w.ckv, w.kpe, table, sel, w.scale, lib=lib)
     assert np.array_equal(out.reshape(o2.shape), o2) and np.array_equal(lse.reshape(l2.shape), l2)
+
+
+def _partial(w, lib):
+    return oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, w.ckv_scale,
+                          w.kpe_scale, lib=lib, tokens=w.tokens)
+
+
+def pin_bruteforce_tokens(lib):
+    """Single-token selections (an indexer's top-k tokens): ids anywhere in
+    the chunk, duplicates, interleaved empty slots, a job with nothing."""
+    w = W.random_case(15, R=3, Mq=2, H=2, P=7, NB=3, K=24, n_valid=[24, 0, 9], allow_dup=True,
+                      pad_pattern="interleaved", tokens=True)
+    assert w.sel.max() >= 64 and (w.sel % 64 != 0).any()
+    out, lse = _partial(w, lib)
+    _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
+def pin_bruteforce_tokens_per_row(lib):
+    """Token selections per query row."""
+    w = W.random_case(16, R=1, Mq=3, H=2, P=6, NB=2, K=10, allow_dup=True, per_row=True,
+                      tokens=True)
+    out, lse = _partial(w, lib)
+    _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
+def pin_tokens_cover_blocks(lib):
+    """Listing all 64 tokens of every selected block, in a shuffled order,
+    equals selecting the blocks (the token path decodes block s // 64 and
+    token s % 64)."""
+    w = W.random_case(17, R=2, Mq=2, H=3, P=10, NB=6, K=3, sigma=0.7)
+    out_b, lse_b = _partial(w, lib)
+    rng = np.random.default_rng(17)
+    tok = np.stack([rng.permutation((w.sel[r][:, None] * BLOCK + np.arange(BLOCK)).ravel())
+                    for r in range(w.sel.shape[0])]).astype(np.int32)
+    wt = W.Workload("tok", w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, tok, w.scale, tokens=True)
+    out_t, lse_t = _partial(wt, lib)
+    np.testing.assert_allclose(lse_t, lse_b, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(out_t, out_b, rtol=1e-11, atol=1e-13)
+
+
+def pin_single_token(lib):
+    """One selected token: its value row comes back exactly and lse is its
+    score; the same token twice adds ln 2 to lse."""
+    w = W.random_case(18, R=1, Mq=1, H=3, P=5, NB=4, K=2)
+    s_id = 2 * BLOCK + 37
+    one = np.array([[s_id, -1]], np.int32)
+    wt = W.Workload("one", w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, one, w.scale, tokens=True)
+    out, lse = _partial(wt, lib)
+    b = int(w.table[0, 2])
+    ckv = W.bf16_bits_to_f32(w.ckv[b, 37]).astype(np.float64)
+    kpe = W.bf16_bits_to_f32(w.kpe[b, 37]).astype(np.float64)
+    for h in range(3):
+        ql = W.bf16_bits_to_f32(w.q_lat[0, 0, h]).astype(np.float64)
+        qp = W.bf16_bits_to_f32(w.q_pe[0, 0, h]).astype(np.float64)
+        score = w.scale * math.fsum(list(ql * ckv) + list(qp * kpe))
+        assert abs(lse[0, 0, h] - score) < 1e-12
+        assert np.array_equal(out[0, 0, h], ckv)
+    wt.sel = np.array([[s_id, s_id]], np.int32)
+    out2, lse2 = _partial(wt, lib)
+    np.testing.assert_allclose(lse2, lse + math.log(2), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(out2, out, rtol=1e-15, atol=0)
 
 
 # ------------------------------------------------------------ library special case
@@ -427,7 +491,8 @@ def pin_e4m3_decode(lib):
 
 
 ALL_PINS = [pin_bf16_decode, pin_e4m3_decode, pin_bruteforce_tiny, pin_bruteforce_multi,
-            pin_bruteforce_per_row, pin_per_row_is_one_job_per_row,
+            pin_bruteforce_per_row, pin_per_row_is_one_job_per_row, pin_bruteforce_tokens,
+            pin_bruteforce_tokens_per_row, pin_tokens_cover_blocks, pin_single_token,
             pin_bruteforce_fp8, pin_dense_equals_library, pin_identical_tokens,
             pin_identical_keys_mean, pin_zero_query, pin_two_groups, pin_one_hot,
             pin_empty_and_duplicates, pin_merge_partition, pin_merge_algebra,

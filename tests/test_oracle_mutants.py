@@ -26,7 +26,15 @@ MUTANTS = [
     ("no_scale", "score[n] = scale * dot;", "score[n] = dot;"),
     ("log2_lse", "double L = M + log(l);", "double L = M + log2(l);"),
     ("unnormalised_weights", "double w = exp(score[k] - L);", "double w = exp(score[k] - M);"),
-    ("skip_block_table", "int64_t b = table[(int64_t)r * NB + s];", "int64_t b = s;"),
+    ("skip_block_table",
+     "int64_t b = table[(int64_t)r * NB + (sel_tokens ? s / ORACLE_BLOCK : s)];",
+     "int64_t b = (sel_tokens ? s / ORACLE_BLOCK : s);"),
+    ("token_offset_dropped", "int t0 = sel_tokens ? s % ORACLE_BLOCK : 0;", "int t0 = 0;"),
+    ("token_block_is_id",
+     "int64_t b = table[(int64_t)r * NB + (sel_tokens ? s / ORACLE_BLOCK : s)];",
+     "int64_t b = table[(int64_t)r * NB + (sel_tokens ? s % NB : s)];"),
+    ("token_whole_block", "const int per_slot = sel_tokens ? 1 : ORACLE_BLOCK;",
+     "const int per_slot = sel_tokens ? 2 : ORACLE_BLOCK;"),
     ("per_row_reads_row0",
      "const int32_t* row_sel = sel + (int64_t)r * sel_s0 + (int64_t)i * sel_s1;",
      "const int32_t* row_sel = sel + (int64_t)r * sel_s0;"),
