@@ -71,9 +71,8 @@ def algorithmic(w):
     """(FLOP, bytes) of one partial-attention launch over workload w."""
     R, Mq, H, _ = w.q_lat.shape
     rows = R * Mq * H
-    nblk = int((w.sel >= 0).sum())
     flops = w.algorithmic_flops()
-    kv = nblk * BLOCK * (DLAT + DPE) * (1 if w.fp8 else 2) + (nblk * 8 if w.fp8 else 0)
+    kv = w.kv_bytes()  # the selected entries (blocks shared by query rows once)
     q = rows * (DLAT + DPE) * 2
     out = rows * (DLAT + 1) * 4
     return flops, kv + q + out, kv
@@ -109,7 +108,8 @@ def main():
     stream = torch.cuda.Stream()
     partial = mla.prepare_partial(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"],
                                   t["sel"], w.scale, out_lat, out_lse, t["ckv_scale"],
-                                  t["kpe_scale"], n_splits=args.n_splits, stream=stream)
+                                  t["kpe_scale"], n_splits=args.n_splits, stream=stream,
+                                  tokens=w.tokens)
     merge = (mla.prepare_merge(part_lat, part_lse, out=merged, stream=stream)
              if merged is not None else (lambda: None))
     torch.cuda.synchronize()
@@ -187,7 +187,8 @@ def main():
             js, ri = jobs_of(reqs)
             sel = w.sel[js][:, ri] if w.sel.ndim == 3 else w.sel[js]
             return (js, ri), oracle.partial(w.q_lat[js][:, ri], w.q_pe[js][:, ri], w.ckv, w.kpe,
-                                            w.table[js], sel, w.scale, w.ckv_scale, w.kpe_scale)
+                                            w.table[js], sel, w.scale, w.ckv_scale, w.kpe_scale,
+                                            tokens=w.tokens)
 
         ts = time.perf_counter()
         js, (o1, l1) = run_oracle([0])
@@ -242,7 +243,8 @@ def main():
         "dtype": "fp8-e4m3 kv, bf16 mfma" if w.fp8 else "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "requests": n_req, "jobs": R, "mq": Mq, "heads": H,
-                   "selected_blocks": int((w.sel >= 0).sum()), "block_tokens": BLOCK,
+                   ("selected_tokens" if w.tokens else "selected_blocks"): int((w.sel >= 0).sum()),
+                   "block_tokens": BLOCK,
                    "pool_blocks": int(w.ckv.shape[0]), "merge_parts": parts},
         "tflops": tflops,
         "pct_bf16_mfma_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,

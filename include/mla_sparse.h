@@ -154,6 +154,35 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
                                         const mla_partial_opts_t* opts, void* stream);
 
 /*
+ * The same partial attention over single selected tokens: an indexer's top-k
+ * tokens of the chunk (the selection budgets of Section 6.3, k = 512 .. 2048
+ * attended entries) rather than whole 64-token blocks.
+ *
+ *   sel_token_ids     [R, K]  int32   selected logical tokens of job r's chunk:
+ *                                     id s names token s % 64 of logical
+ *                                     block s / 64, i.e. pool token
+ *                                     chunk_block_table[r, s / 64] * 64 + s % 64;
+ *                                     -1 marks an empty slot; a token listed
+ *                                     twice counts twice
+ *
+ * Every other argument, the result (T = the multiset of selected tokens)
+ * and the layout rules are those of mla_sparse_partial_attn_ex; opts.n_splits
+ * counts splits of the token slots (each split takes whole 64-token groups
+ * of slots, at most 1024 slots).  bf16 caches only (MLA_ERR_UNSUPPORTED for
+ * fp8); NB and P must not exceed 2^25 blocks (MLA_ERR_UNSUPPORTED).  An id
+ * outside [0, 64 NB), or a table entry outside [0, P), is a caller error that
+ * the call does not detect on the host: such a slot is skipped.
+ */
+mla_status_t mla_sparse_partial_attn_tokens(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                            const mla_tensor_t* ckv_pool,
+                                            const mla_tensor_t* kpe_pool,
+                                            const mla_tensor_t* chunk_block_table,
+                                            const mla_tensor_t* sel_token_ids, float scale,
+                                            const mla_tensor_t* out_lat,
+                                            const mla_tensor_t* out_lse,
+                                            const mla_partial_opts_t* opts, void* stream);
+
+/*
  * Log-sum-exp merge of n_parts partials of the same rows (the requester's
  * online-softmax recombination, Sections 2.2, 3.3 and 4.2).
  *

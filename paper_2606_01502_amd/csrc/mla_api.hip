@@ -135,20 +135,14 @@ int device_cus() {
   return cus;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* mla_last_error(void) { return g_last_error.c_str(); }
-
-int32_t mla_version(void) { return MLA_SPARSE_VERSION; }
-
-mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
-                                        const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
-                                        const mla_tensor_t* chunk_block_table,
-                                        const mla_tensor_t* sel_block_ids, float scale,
-                                        const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
-                                        const mla_partial_opts_t* opts, void* stream) {
+// The partial call; `tokens`: sel names single logical tokens (block * 64 +
+// t) rather than blocks.
+mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                          const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                          const mla_tensor_t* chunk_block_table,
+                          const mla_tensor_t* sel_block_ids, float scale,
+                          const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                          const mla_partial_opts_t* opts, void* stream, bool tokens) {
   try {
     g_last_error.clear();
     mla_status_t st;
@@ -164,8 +158,9 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (fp8 && (!ckv_pool->block_scale || !kpe_pool->block_scale))
       return fail(MLA_ERR_INVALID_ARGUMENT, "fp8 pools need block_scale");
     if ((st = check_tensor(chunk_block_table, "chunk_block_table", MLA_DTYPE_INT32, 2)) != MLA_OK) return st;
-    const bool per_row = sel_block_ids && sel_block_ids->ndim == 3;
-    if ((st = check_tensor(sel_block_ids, "sel_block_ids", MLA_DTYPE_INT32, per_row ? 3 : 2)) != MLA_OK)
+    const bool per_row = !tokens && sel_block_ids && sel_block_ids->ndim == 3;
+    const char* sel_name = tokens ? "sel_token_ids" : "sel_block_ids";
+    if ((st = check_tensor(sel_block_ids, sel_name, MLA_DTYPE_INT32, per_row ? 3 : 2)) != MLA_OK)
       return st;
     if ((st = check_tensor(out_lat, "out_lat", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
     if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
@@ -195,6 +190,8 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K] or [R, Mq, K]");
     if (per_row && fp8)
       return fail(MLA_ERR_UNSUPPORTED, "per-row selections need a bf16 cache");
+    if (tokens && fp8)
+      return fail(MLA_ERR_UNSUPPORTED, "token selections need a bf16 cache");
     if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
     if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
     if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||
@@ -208,6 +205,8 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     if (!std::isfinite(scale)) return fail(MLA_ERR_INVALID_ARGUMENT, "scale must be finite");
     if (R > INT32_MAX || Mq * H > (1 << 24) || K > INT32_MAX || NB > INT32_MAX || P > INT32_MAX)
       return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the int32 index range");
+    if (tokens && (NB > (INT32_MAX >> 6) || P > (INT32_MAX >> 6)))
+      return fail(MLA_ERR_UNSUPPORTED, "token selections: NB or P beyond 2^25 blocks");
 
     const Extent outs[2] = {extent(*out_lat), extent(*out_lse)};
     auto scale_extent = [&](const float* sc) -> Extent {
@@ -227,6 +226,8 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
 
     // ---- plan: row tiles of 128 or 64 rows (4 waves of 32 or 16 rows);
     // split-K over slot ranges so that the grid covers the chip
+    // slots in 64-token blocks (a token selection's slots fill K / 64 blocks)
+    const int64_t Kb = tokens ? (K + 63) / 64 : K;
     int row_groups = rows > 64 ? 2 : 1;
     if (opts && opts->row_tile) {
       row_groups = opts->row_tile / 64;
@@ -238,8 +239,8 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       // rows out)
       const int64_t units2 = R * ((rows + 127) / 128);
       const int64_t s2 = std::min<int64_t>((device_cus() + units2 - 1) / units2,
-                                           std::max<int64_t>(K / 2, 1));
-      if (K < 8 * s2) row_groups = 1;
+                                           std::max<int64_t>(Kb / 2, 1));
+      if (Kb < 8 * s2) row_groups = 1;
     }
     // per-row selections: the query rows a row tile spans (one mask bit each)
     auto tile_query_rows = [&](int rg) {
@@ -283,12 +284,18 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
       // epilogue and share of the combine) than the block itself
       const int64_t units = R * row_tiles;
       S = std::max<int64_t>(1, (device_cus() + units - 1) / units);
-      S = std::min<int64_t>(S, std::max<int64_t>(K / 2, 1));
+      S = std::min<int64_t>(S, std::max<int64_t>(Kb / 2, 1));
     }
     // a split's block list holds at most kMaxSlotsPerSplit entries: its slots,
     // or for per-row selections its slots of every query row of the tile
     int64_t sps = K;
-    if (!by_id) {
+    if (tokens) {
+      // whole virtual blocks per split, at most one list of tokens
+      S = std::max<int64_t>(S, (K + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
+      sps = std::max<int64_t>(64, ((K + S - 1) / S + 63) / 64 * 64);
+      sps = std::min<int64_t>(sps, mla::kMaxSlotsPerSplit);
+      S = std::max<int64_t>(1, (K + sps - 1) / sps);
+    } else if (!by_id) {
       S = std::max<int64_t>(S, (K * tile_qrows + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
       sps = std::max<int64_t>(1, (K + S - 1) / S);
       if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, mla::kMaxSlotsPerSplit / tile_qrows));
@@ -337,7 +344,8 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
     const int kv = !fp8 ? mla::kKvBf16
                  : (ckv_pool->block_scale == kpe_pool->block_scale ? mla::kKvFp8Shared
                                                                    : mla::kKvFp8Split);
-    hipError_t e = mla::launch_partial(p, (int)R, kv, row_groups, per_row, hs);
+    const int sel_kind = tokens ? mla::kSelTokens : per_row ? mla::kSelPerRow : mla::kSelShared;
+    hipError_t e = mla::launch_partial(p, (int)R, kv, row_groups, sel_kind, hs);
     if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
     if (S > 1) {
       mla::CombineParams c{};
@@ -353,6 +361,36 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
   } catch (...) {
     return fail(MLA_ERR_HIP, "internal error");
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mla_last_error(void) { return g_last_error.c_str(); }
+
+int32_t mla_version(void) { return MLA_SPARSE_VERSION; }
+
+mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                        const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                                        const mla_tensor_t* chunk_block_table,
+                                        const mla_tensor_t* sel_block_ids, float scale,
+                                        const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
+                                        const mla_partial_opts_t* opts, void* stream) {
+  return partial_call(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
+                      out_lat, out_lse, opts, stream, false);
+}
+
+mla_status_t mla_sparse_partial_attn_tokens(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                            const mla_tensor_t* ckv_pool,
+                                            const mla_tensor_t* kpe_pool,
+                                            const mla_tensor_t* chunk_block_table,
+                                            const mla_tensor_t* sel_token_ids, float scale,
+                                            const mla_tensor_t* out_lat,
+                                            const mla_tensor_t* out_lse,
+                                            const mla_partial_opts_t* opts, void* stream) {
+  return partial_call(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, scale,
+                      out_lat, out_lse, opts, stream, true);
 }
 
 mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,

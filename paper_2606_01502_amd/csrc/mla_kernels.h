@@ -81,10 +81,15 @@ constexpr int kKvFp8Split = 2;   // e4m3, separate ckv and kpe scales per block
 constexpr int kPerRowCounterBytes = 2 * 64 * 1152;  // the bf16 stage area
 constexpr int kPerRowMaxRows = 64;                  // query rows per row tile (mask bits)
 
+// Selection kinds: one block selection per job, one per query row, or one
+// token selection per job (bf16 caches only for the last two).
+constexpr int kSelShared = 0;
+constexpr int kSelPerRow = 1;
+constexpr int kSelTokens = 2;
+
 // Launchers; return hipSuccess or the launch error.
-// row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows);
-// per_row: sel holds a selection per query row (bf16 caches only)
-hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, bool per_row,
+// row_groups: 2 (row tiles of 128 rows) or 1 (row tiles of 64 rows)
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, int sel_kind,
                           hipStream_t s);
 hipError_t launch_combine(const CombineParams& p, hipStream_t s);
 hipError_t launch_merge(const MergeParams& p, hipStream_t s);

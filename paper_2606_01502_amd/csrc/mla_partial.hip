@@ -401,6 +401,37 @@ struct Bf16Issue {
   }
 };
 
+// The bf16 loads of a virtual block of 64 listed tokens (token selections),
+// into the same stage layout as a pool block: latent load j of wave w is the
+// 1 KiB row of the stage's token 16w + j, read from that token's row of the
+// pool (a scalar base per load); RoPE loads 16, 17 are the stage's tokens
+// 16w .. 16w+7 and 16w+8 .. 16w+15, a per-lane address each.
+struct TokIssue {
+  int tok;             // pool token (block * 64 + t) of stage token 16w + (lane & 15)
+  uint32_t m0;         // LDS address of row 16w of the stage
+  uint32_t lds_rope;   // LDS address of the stage's RoPE part + 2 KiB * w
+  __device__ __forceinline__ void load(const PartialParams& p, int j, int wave, int lane_in) const {
+    if (j < 16) {
+      const uint32_t t = (uint32_t)__builtin_amdgcn_readlane(tok, j);
+      const uint8_t* row = p.ckv + (uint64_t)t * 1024u;
+      const uint32_t off = ((uint32_t)lds_opaque(lane_in) << 4) ^ (uint32_t)(j << 4);
+      asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                   :: "v"(off), "s"(row), "s"(m0 + (uint32_t)j * 1024u) : "memory", "m0");
+    } else {
+      int lane;
+      asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
+      const int src = 8 * (j - 16) + (lane >> 3);  // the lane's token among the wave's 16
+      const int t = __shfl(tok, src);
+      const int row = 16 * wave + src;             // its row in the stage (swizzle key)
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      const uint8_t* a = p.kpe + (uint64_t)(uint32_t)t * 128u + (uint32_t)(c << 4);
+      const uint32_t d = __builtin_amdgcn_readfirstlane(lds_rope + (uint32_t)(j - 16) * 1024u);
+      asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                   :: "v"(a), "s"(d) : "memory", "m0");
+    }
+  }
+};
+
 // Wait until at most `stages` later stages of this wave's loads are in flight.
 template <bool FP8>
 __device__ __forceinline__ void wait_stages(int stages) {
@@ -595,15 +626,65 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
   return n_valid;
 }
 
+// Token selections: compact the valid token ids of slots [slot0, slot0 +
+// nslots) of job r into the LDS list as pool tokens (table[r, id / 64] * 64 +
+// id % 64), slot order kept, and fill the list up to the next multiple of 64
+// with the first entry, so that the last virtual block loads only listed
+// tokens (the fill is masked out of the softmax).  Returns the number of
+// listed tokens.
+__device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int slot0,
+                                              int nslots, LDS uint8_t* smem, int tid) {
+  using L = Layout<false>;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  LDS int* list = (LDS int*)(smem + L::kList);
+  LDS int* wave_cnt = (LDS int*)(smem + L::kWaveCnt);
+  const int64_t n_ids = (int64_t)p.NB * kBlock;
+  int n_tok = 0;
+  for (int base = 0; base < nslots; base += 256) {
+    const int i = base + tid;
+    int pt = -1;
+    if (i < nslots) {
+      const int id = p.sel[r * p.sel_s0 + slot0 + i];
+      if (id >= 0 && id < n_ids) {
+        const int bb = p.table[r * p.table_s0 + (id >> 6)];
+        if (bb >= 0 && bb < p.P) pt = bb * kBlock + (id & (kBlock - 1));
+      }
+    }
+    const uint64_t m = __ballot(pt >= 0);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[wave] = __popcll(m);
+    lds_barrier();
+    int off = n_tok, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = wave_cnt[w];
+      off += (w < wave) ? c : 0;
+      total += c;
+    }
+    if (pt >= 0) list[off + before] = pt;
+    n_tok += total;
+    lds_barrier();
+  }
+  const int padded = (n_tok + kBlock - 1) & ~(kBlock - 1);
+  if (tid >= n_tok && tid < padded) list[tid] = list[0];
+  for (int i = tid + 256; i < padded; i += 256)
+    if (i >= n_tok) list[i] = list[0];
+  lds_barrier();
+  return n_tok;
+}
+
 // RG row groups of 16 per wave: wave w computes rows 16*RG*w .. 16*RG*(w+1)-1
 // of the row tile (64*RG rows) over all 512 latent columns.  KV is the cache
 // kind: bf16, e4m3 with one scale per block for the whole 576-wide entries, or
 // e4m3 with separate latent and RoPE scales per block.
-template <int RG, int KV, bool PR>
+template <int RG, int KV, int SEL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void partial_kernel(const PartialParams p) {
   constexpr bool FP8 = KV != kKvBf16;
-  static_assert(!(PR && FP8), "per-row selections: bf16 caches only");
+  constexpr bool PR = SEL == kSelPerRow;   // a block selection per query row
+  constexpr bool TOK = SEL == kSelTokens;  // token selections, 64 to a virtual block
+  static_assert(!((PR || TOK) && FP8), "per-row and token selections: bf16 caches only");
   constexpr bool kSplitScales = KV == kKvFp8Split;
   using L = Layout<FP8>;
   constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
@@ -634,6 +715,7 @@ void partial_kernel(const PartialParams p) {
   LDS uint64_t* masks = (LDS uint64_t*)(smem + L::kMasks);
   const int i0 = rt * kRowsWg / p.H;  // first query row of the tile
   int n_valid;
+  int n_tok = 0;  // token selections: the listed tokens (n_valid counts virtual blocks)
   if constexpr (PR) {
     const int n_i = (min((rt + 1) * kRowsWg, p.rows) - 1) / p.H - i0 + 1;
     // split by logical block (split s takes blocks s, s + S, ... from every
@@ -642,14 +724,29 @@ void partial_kernel(const PartialParams p) {
     n_valid = p.split_by_id
                   ? compact_per_row(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
                   : compact_per_row(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
+  } else if constexpr (TOK) {
+    n_tok = compact_tokens(p, r, slot0, nslots, smem, tid);
+    n_valid = (n_tok + kBlock - 1) / kBlock;
   } else {
     n_valid = compact_slots<FP8>(p, r, slot0, nslots, smem, tid);
   }
 
   // ---- the first blocks' loads go out before the query rows, so that their
   // latencies overlap
-  for (int h = 0; h < n_valid && h < L::kLead; ++h)
-    issue_stage<FP8>(p, list[h], stage0 + h * L::kStage, wave, lane);
+  if constexpr (TOK) {
+    static_assert(L::kLead == 1, "token selections stream one virtual block ahead");
+    if (n_valid > 0) {
+      TokIssue ti;
+      ti.tok = list[16 * wave + (lane & 15)];
+      ti.m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)stage0 + (uint32_t)wave * 16384u);
+      ti.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)stage0 + 65536u + (uint32_t)wave * 2048u);
+#pragma unroll
+      for (int j = 0; j < L::kLoads; ++j) ti.load(p, j, wave, lane);
+    }
+  } else {
+    for (int h = 0; h < n_valid && h < L::kLead; ++h)
+      issue_stage<FP8>(p, list[h], stage0 + h * L::kStage, wave, lane);
+  }
 
   // ---- this wave's query rows as MFMA B operands, held for the whole kernel:
   // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
@@ -705,7 +802,7 @@ void partial_kernel(const PartialParams p) {
     // The pool block that streams into the stage freed by this block (read
     // from LDS first: LDS reads complete in order).
     const int hn = h + L::kLead;
-    const int b_next = hn < n_valid ? __builtin_amdgcn_readfirstlane(list[hn]) : -1;
+    const int b_next = hn >= n_valid ? -1 : TOK ? 0 : __builtin_amdgcn_readfirstlane(list[hn]);
     uint64_t emask = ~0ull;  // the rows this entry is attended by
     if constexpr (PR) {
       // (readfirstlane returns int: widen through uint32_t, not by sign)
@@ -732,8 +829,12 @@ void partial_kernel(const PartialParams p) {
     // the per-CU address unit, which takes one 1 KiB load per ~16 cycles).
     // fp8 (9 loads): all at once after the first key reads.
     LDS uint8_t* const next_buf = stage0 + (hn % L::kNum) * L::kStage;
-    Bf16Issue bi;
-    if constexpr (!FP8) {
+    typename std::conditional<TOK, TokIssue, Bf16Issue>::type bi;
+    if constexpr (TOK) {
+      bi.tok = b_next >= 0 ? list[hn * kBlock + 16 * wave + (lane & 15)] : 0;
+      bi.m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + (uint32_t)wave * 16384u);
+      bi.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + 65536u + (uint32_t)wave * 2048u);
+    } else if constexpr (!FP8) {
       const int64_t bn = b_next >= 0 ? b_next : 0;
       bi.ckv = p.ckv + bn * 65536 + wave * 16384;
       bi.kpe = p.kpe + bn * 8192;
@@ -919,12 +1020,20 @@ void partial_kernel(const PartialParams p) {
     // holds row n16 of each row group and tokens 16*tau + 4g + i.
     bool need_any = false;
     float bmax[RG];
+    // token selections: the listed tokens in this virtual block (the rest of
+    // the last one is fill, with no weight)
+    const int n_here = TOK ? n_tok - h * kBlock : kBlock;
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
       float bm = -INFINITY;
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) {
         acc[rg][tau] *= s_mult;
+        if (TOK && n_here < kBlock) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (16 * tau + 4 * lg + k >= n_here) acc[rg][tau][k] = -INFINITY;
+        }
 #pragma unroll
         for (int k = 0; k < 4; ++k) bm = fmaxf(bm, acc[rg][tau][k]);
       }
@@ -1070,21 +1179,24 @@ void partial_kernel(const PartialParams p) {
 
 }  // namespace
 
-template <int KV, bool PR = false>
+template <int KV, int SEL = kSelShared>
 static void launch_kv(const PartialParams& p, int grid, int row_groups, hipStream_t s) {
   if (row_groups == 2)
-    hipLaunchKernelGGL((partial_kernel<2, KV, PR>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_kernel<2, KV, SEL>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((partial_kernel<1, KV, PR>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((partial_kernel<1, KV, SEL>), dim3(grid), dim3(256), 0, s, p);
 }
 
-hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, bool per_row,
+hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups, int sel_kind,
                           hipStream_t s) {
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (per_row) {
+  if (sel_kind == kSelPerRow || sel_kind == kSelTokens) {
     if (kv != kKvBf16) return hipErrorInvalidValue;
-    launch_kv<kKvBf16, true>(p, grid, row_groups, s);
+    if (sel_kind == kSelPerRow)
+      launch_kv<kKvBf16, kSelPerRow>(p, grid, row_groups, s);
+    else
+      launch_kv<kKvBf16, kSelTokens>(p, grid, row_groups, s);
   } else if (kv == kKvFp8Shared)
     launch_kv<kKvFp8Shared>(p, grid, row_groups, s);
   else if (kv == kKvFp8Split)

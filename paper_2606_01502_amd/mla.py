@@ -25,8 +25,9 @@ MLA_ERR_OUT_OF_MEMORY = -4
 
 DTYPE_BF16, DTYPE_FP8_E4M3FN, DTYPE_FP32, DTYPE_INT32 = 1, 2, 3, 4
 
-EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex", "mla_merge_partials",
-           "mla_merge_partials_ex", "mla_last_error", "mla_version")
+EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex",
+           "mla_sparse_partial_attn_tokens", "mla_merge_partials", "mla_merge_partials_ex",
+           "mla_last_error", "mla_version")
 
 
 class MlaError(RuntimeError):
@@ -65,6 +66,8 @@ def load(path: str = LIB_PATH):
     lib.mla_sparse_partial_attn_ex.restype = ctypes.c_int
     lib.mla_sparse_partial_attn_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P,
                                                ctypes.POINTER(PartialOpts), vp]
+    lib.mla_sparse_partial_attn_tokens.restype = ctypes.c_int
+    lib.mla_sparse_partial_attn_tokens.argtypes = lib.mla_sparse_partial_attn_ex.argtypes
     lib.mla_merge_partials.restype = ctypes.c_int
     lib.mla_merge_partials.argtypes = [PP, PP, ctypes.c_int32, P, vp]
     lib.mla_merge_partials_ex.restype = ctypes.c_int
@@ -165,20 +168,24 @@ def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_
 
 def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                     out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None, n_splits=0,
-                    row_tile=0, stream=None):
+                    row_tile=0, stream=None, tokens=False):
     """sparse_partial_attn with every argument fixed, the stream included
     (the current one when None); calling the result launches the work and
     returns (out_lat, out_lse)."""
     args, keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                        sel_block_ids, scale, out_lat, out_lse, ckv_scale,
                                        kpe_scale, n_splits, row_tile, stream)
-    return _Prepared(load().mla_sparse_partial_attn_ex, args, keep, result)
+    lib = load()
+    fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
+    return _Prepared(fn, args, keep, result)
 
 
 def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
                         scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
-                        n_splits=0, row_tile=0, stream=None):
-    """Partial attention of each job's Mq x H rows over its selected blocks.
+                        n_splits=0, row_tile=0, stream=None, tokens=False):
+    """Partial attention of each job's Mq x H rows over its selected blocks,
+    or with tokens=True over its selected single tokens (sel_block_ids then
+    holds logical token ids, block * 64 + t).
 
     Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
     """
@@ -186,7 +193,8 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     args, _keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                         sel_block_ids, scale, out_lat, out_lse, ckv_scale,
                                         kpe_scale, n_splits, row_tile, stream)
-    _check(lib, lib.mla_sparse_partial_attn_ex(*args))
+    fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
+    _check(lib, fn(*args))
     return result
 
 

@@ -342,6 +342,36 @@ def holder(n_req, heads, sparse=False, as_jobs=False, seed=7):
                     n_requests=n_req, merge_parts=1)
 
 
+def selection(kind, n_req, k, corpus, heads=128, seed=8):
+    """The selection-regime holder of Section 6.3 at a selection budget of k
+    tokens: n_req requests (Mq = 1, `heads` heads, q ~ N(0,1)), each over a
+    chunk of its own of `corpus` tokens (corpus / 64 blocks ~ N(0,0.5),
+    scattered in the pool).
+      tok:   the top-k as k single tokens drawn uniformly without replacement
+             over the chunk, sorted (a token-level indexer, block = 1);
+      blk:   k / 64 whole blocks drawn uniformly without replacement, sorted;
+      dense: the first k / 64 blocks of the chunk, laid out contiguously in
+             the pool (dense decode over k resident tokens, the matched-k
+             reference of the sparse premium)."""
+    assert k % BLOCK == 0 and corpus % BLOCK == 0 and k <= corpus
+    nb = corpus // BLOCK
+    q_lat, q_pe = _queries(seed, n_req, 1, heads)
+    P = n_req * nb
+    ckv, kpe = _pool(seed, P, 0.5)
+    rs = np.random.default_rng([seed, _T_SEL])
+    if kind == "dense":
+        table = np.arange(P, dtype=np.int32).reshape(n_req, nb)
+        sel = np.tile(np.arange(k // BLOCK, dtype=np.int32), (n_req, 1))
+    else:
+        table = _perm(seed, P).reshape(n_req, nb)
+        n_ids = nb * BLOCK if kind == "tok" else nb
+        m = k if kind == "tok" else k // BLOCK
+        sel = np.stack([np.sort(rs.choice(n_ids, m, replace=False)) for _ in range(n_req)])
+    name = f"select-{kind}-b{n_req}-k{k}-c{corpus}" + ("" if heads == 128 else f"-h{heads}")
+    return Workload(name, q_lat, q_pe, ckv, kpe, table.astype(np.int32), sel.astype(np.int32),
+                    n_requests=n_req, merge_parts=1, tokens=kind == "tok")
+
+
 CONFIGS = {
     "tiny": tiny,
     "dsv3-one-request": dsv3_one_request,
@@ -354,7 +384,15 @@ CONFIGS = {
 
 def make(name, seed=None, **kw):
     """A named workload; `holder-{dense|sparse}-n{N}-h{H}[-jobs]` builds the
-    holder experiment (see holder)."""
+    holder experiment (see holder), `select-{tok|blk|dense}-b{B}-k{k}-c{c}[-h{H}]`
+    the selection-budget experiment (see selection)."""
+    if name.startswith("select-"):
+        parts = name.split("-")
+        kw.update(kind=parts[1], n_req=int(parts[2][1:]), k=int(parts[3][1:]),
+                  corpus=int(parts[4][1:]))
+        if len(parts) > 5:
+            kw.update(heads=int(parts[5][1:]))
+        return selection(**kw) if seed is None else selection(seed=seed, **kw)
     if name.startswith("holder-"):
         parts = name.split("-")
         kw.update(n_req=int(parts[2][1:]), heads=int(parts[3][1:]),

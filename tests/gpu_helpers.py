@@ -42,11 +42,11 @@ def upload(w):
     return t
 
 
-def run_partial(t, scale, n_splits=0, sel=None, row_tile=0):
+def run_partial(t, scale, n_splits=0, sel=None, row_tile=0, tokens=False):
     out, lse = mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"],
                                        t["sel"] if sel is None else sel, scale,
                                        ckv_scale=t["ckv_scale"], kpe_scale=t["kpe_scale"],
-                                       n_splits=n_splits, row_tile=row_tile)
+                                       n_splits=n_splits, row_tile=row_tile, tokens=tokens)
     torch.cuda.synchronize()
     return out.cpu().numpy().astype(np.float64), lse.cpu().numpy().astype(np.float64)
 

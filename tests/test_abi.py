@@ -69,7 +69,7 @@ def test_packed_descriptor_equals_fieldwise():
         assert bytes(mla.describe(t, bs)) == bytes(_describe_fieldwise(t, bs)), (t.shape, t.stride())
 
 
-def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0):
+def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0, tokens=False):
     """Call the partial entry point on CPU tensors: only the host-side checks
     run (each of these calls must fail before anything is launched)."""
     import types
@@ -86,7 +86,7 @@ def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0):
     stream = types.SimpleNamespace(cuda_stream=0)
     try:
         mla.sparse_partial_attn(q_lat, q_pe, ckv, kpe, table, sel, 0.1, ckv_scale=sc,
-                                kpe_scale=sc, row_tile=row_tile, stream=stream)
+                                kpe_scale=sc, row_tile=row_tile, stream=stream, tokens=tokens)
     except mla.MlaError as e:
         return e.status, str(e)
     return mla.MLA_OK, ""
@@ -107,6 +107,16 @@ def test_per_row_selection_host_checks():
     # a 128-row tile of H = 1 spans 128 query rows, more than a row mask holds
     st, msg = _cpu_call((2, 70, 3), Mq=70, H=1, row_tile=128)
     assert st == mla.MLA_ERR_UNSUPPORTED and "128-row" in msg
+
+
+def test_token_selection_host_checks():
+    from paper_2606_01502_amd import mla
+    st, msg = _cpu_call((2, 3), fp8=True, tokens=True)
+    assert st == mla.MLA_ERR_UNSUPPORTED and "bf16" in msg
+    st, msg = _cpu_call((2, 3, 3), tokens=True)  # no per-row token selections
+    assert st == mla.MLA_ERR_INVALID_ARGUMENT and "sel_token_ids" in msg
+    st, msg = _cpu_call((3, 3), tokens=True)  # R mismatch
+    assert st == mla.MLA_ERR_INVALID_ARGUMENT
 
 
 def test_row_tile_option_checked():
