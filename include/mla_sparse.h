@@ -216,6 +216,63 @@ const char* mla_last_error(void);
 /* MLA_SPARSE_VERSION of the loaded library. */
 int32_t mla_version(void);
 
+/*
+ * The closed-form cost model of the three redistribution primitives and the
+ * selection predicate (Sections 4.1-4.2 and 5.1-5.2).  Host-only arithmetic:
+ * no device, no stream; a scheduler evaluates it per (chunk, request).
+ * Times in microseconds, throughputs in GB/s (1e9 bytes per second), sizes
+ * in bytes.  The paper's measured constants are given in brackets.
+ */
+typedef struct {
+  double probe_us;     /* T_probe(F): the fabric's signalled round trip [16]      */
+  double route_bw_gbs; /* BW(F): routing's effective bidirectional throughput [25] */
+  double compute_us;   /* T_compute: the holder's partial attention (0: transport
+                          only, as the paper's fitted round trip)                */
+  double merge_us;     /* T_merge: the requester's merge (0: transport only)      */
+  double pull_bw_gbs;  /* FETCH's bulk pull throughput [25]                       */
+  double splice_us;    /* T_splice: FETCH's position adaptation [3000]; 0 under
+                          sparse selection                                       */
+  double prefill_us;   /* c: LOCAL's re-prefill cost per token and layer
+                          [0.5 .. 1.5]                                           */
+  int32_t layers;      /* L: layers FETCH pulls and LOCAL re-prefills [27]        */
+  int32_t reserved;    /* must be zero                                           */
+} mla_cost_model_t;
+
+typedef struct {
+  int64_t mq;           /* Mq: query rows routed to the chunk                    */
+  int64_t chunk_tokens; /* c_t: tokens of the chunk                               */
+  int64_t q_bytes;      /* q: bytes per routed query row [576 x 2 = 1152]         */
+  int64_t p_bytes;      /* p: bytes per returned partial row [512 x 2 + 2 x 4 =
+                           1032]                                                  */
+  int64_t kv_bytes;     /* b_KV: cached bytes per token and layer [1152]          */
+} mla_cost_case_t;
+
+enum { MLA_PRIMITIVE_ROUTE = 0, MLA_PRIMITIVE_FETCH = 1, MLA_PRIMITIVE_LOCAL = 2 };
+
+typedef struct {
+  double route_us;  /* T_probe + Mq (q + p) / BW + T_compute + T_merge            */
+  double fetch_us;  /* L c_t b_KV / pull BW + T_splice                            */
+  double local_us;  /* c_t L c                                                     */
+  int32_t choice;   /* the argmin: MLA_PRIMITIVE_*; ties go to ROUTE, then FETCH   */
+  int32_t reserved;
+  double wire_crossover_mq;       /* Mq at which routing and pulling one layer move
+                                     equal bytes: c_t b_KV / (q + p)               */
+  double wire_saving;             /* 1 - Mq (q + p) / (c_t b_KV): the share of one
+                                     layer's pull bytes routing does not move      */
+  double congestion_bw_gbs;       /* BW below which routing's transfer exceeds the
+                                     splice: Mq (q + p) / T_splice (inf if no
+                                     splice)                                       */
+  double splice_crossover_tokens; /* c_t above which the splice undercuts
+                                     re-prefill: T_splice / (L c) (inf if c = 0)   */
+} mla_cost_t;
+
+/* Evaluate the model for one case.  MLA_ERR_INVALID_ARGUMENT for a null
+ * pointer, a negative or non-finite constant, a non-positive throughput, a
+ * negative size, layers < 1, chunk_tokens or kv_bytes of 0, or nonzero
+ * reserved fields. */
+mla_status_t mla_primitive_costs(const mla_cost_model_t* model, const mla_cost_case_t* c,
+                                 mla_cost_t* out);
+
 #ifdef __cplusplus
 }
 #endif

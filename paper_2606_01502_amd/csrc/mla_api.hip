@@ -393,6 +393,41 @@ mla_status_t mla_sparse_partial_attn_tokens(const mla_tensor_t* q_lat, const mla
                       out_lat, out_lse, opts, stream, true);
 }
 
+mla_status_t mla_primitive_costs(const mla_cost_model_t* m, const mla_cost_case_t* c,
+                                 mla_cost_t* out) {
+  g_last_error.clear();
+  if (!m || !c || !out) return fail(MLA_ERR_INVALID_ARGUMENT, "null pointer");
+  const double consts[] = {m->probe_us, m->compute_us, m->merge_us, m->splice_us, m->prefill_us};
+  for (double v : consts)
+    if (!(v >= 0.0) || !std::isfinite(v))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "model times must be finite and >= 0");
+  if (!(m->route_bw_gbs > 0.0) || !(m->pull_bw_gbs > 0.0) || !std::isfinite(m->route_bw_gbs) ||
+      !std::isfinite(m->pull_bw_gbs))
+    return fail(MLA_ERR_INVALID_ARGUMENT, "throughputs must be finite and > 0");
+  if (m->layers < 1 || m->reserved) return fail(MLA_ERR_INVALID_ARGUMENT, "layers must be >= 1, reserved 0");
+  if (c->mq < 0 || c->q_bytes < 0 || c->p_bytes < 0 || c->chunk_tokens < 1 || c->kv_bytes < 1)
+    return fail(MLA_ERR_INVALID_ARGUMENT, "sizes: mq, q, p >= 0; chunk_tokens, kv_bytes >= 1");
+  // bytes / (GB/s) = 1e-9 s per byte = 1e-3 us per byte
+  const double row = (double)c->q_bytes + (double)c->p_bytes;  // q + p, one routed row
+  const double routed = (double)c->mq * row;                    // Mq (q + p)
+  const double layer_chunk = (double)c->chunk_tokens * (double)c->kv_bytes;  // c_t b_KV
+  const double L = (double)m->layers;
+  mla_cost_t r{};
+  r.route_us = m->probe_us + routed / (m->route_bw_gbs * 1e3) + m->compute_us + m->merge_us;
+  r.fetch_us = L * layer_chunk / (m->pull_bw_gbs * 1e3) + m->splice_us;
+  r.local_us = (double)c->chunk_tokens * L * m->prefill_us;
+  r.choice = MLA_PRIMITIVE_ROUTE;
+  double best = r.route_us;
+  if (r.fetch_us < best) { r.choice = MLA_PRIMITIVE_FETCH; best = r.fetch_us; }
+  if (r.local_us < best) r.choice = MLA_PRIMITIVE_LOCAL;
+  r.wire_crossover_mq = row > 0.0 ? layer_chunk / row : INFINITY;
+  r.wire_saving = 1.0 - routed / layer_chunk;
+  r.congestion_bw_gbs = m->splice_us > 0.0 ? routed / (m->splice_us * 1e3) : INFINITY;
+  r.splice_crossover_tokens = m->prefill_us > 0.0 ? m->splice_us / (L * m->prefill_us) : INFINITY;
+  *out = r;
+  return MLA_OK;
+}
+
 mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
                                      const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
                                      const mla_tensor_t* chunk_block_table,

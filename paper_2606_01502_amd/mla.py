@@ -27,7 +27,7 @@ DTYPE_BF16, DTYPE_FP8_E4M3FN, DTYPE_FP32, DTYPE_INT32 = 1, 2, 3, 4
 
 EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex",
            "mla_sparse_partial_attn_tokens", "mla_merge_partials", "mla_merge_partials_ex",
-           "mla_last_error", "mla_version")
+           "mla_last_error", "mla_version", "mla_primitive_costs")
 
 
 class MlaError(RuntimeError):
@@ -40,6 +40,34 @@ class Tensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
                 ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4),
                 ("block_scale", ctypes.c_void_p)]
+
+
+class CostModel(ctypes.Structure):
+    _fields_ = [("probe_us", ctypes.c_double), ("route_bw_gbs", ctypes.c_double),
+                ("compute_us", ctypes.c_double), ("merge_us", ctypes.c_double),
+                ("pull_bw_gbs", ctypes.c_double), ("splice_us", ctypes.c_double),
+                ("prefill_us", ctypes.c_double), ("layers", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class CostCase(ctypes.Structure):
+    _fields_ = [("mq", ctypes.c_int64), ("chunk_tokens", ctypes.c_int64),
+                ("q_bytes", ctypes.c_int64), ("p_bytes", ctypes.c_int64),
+                ("kv_bytes", ctypes.c_int64)]
+
+
+class Cost(ctypes.Structure):
+    _fields_ = [("route_us", ctypes.c_double), ("fetch_us", ctypes.c_double),
+                ("local_us", ctypes.c_double), ("choice", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("wire_crossover_mq", ctypes.c_double),
+                ("wire_saving", ctypes.c_double), ("congestion_bw_gbs", ctypes.c_double),
+                ("splice_crossover_tokens", ctypes.c_double)]
+
+
+PRIMITIVES = ("route", "fetch", "local")
+# the constants the paper measured (Sections 4.3 and 5.1; c in [0.5, 1.5])
+PAPER_COST_MODEL = dict(probe_us=16.0, route_bw_gbs=25.0, compute_us=0.0, merge_us=0.0,
+                        pull_bw_gbs=25.0, splice_us=3000.0, prefill_us=1.0, layers=27)
 
 
 class PartialOpts(ctypes.Structure):
@@ -72,6 +100,9 @@ def load(path: str = LIB_PATH):
     lib.mla_merge_partials.argtypes = [PP, PP, ctypes.c_int32, P, vp]
     lib.mla_merge_partials_ex.restype = ctypes.c_int
     lib.mla_merge_partials_ex.argtypes = [PP, PP, ctypes.c_int32, P, P, vp]
+    lib.mla_primitive_costs.restype = ctypes.c_int
+    lib.mla_primitive_costs.argtypes = [ctypes.POINTER(CostModel), ctypes.POINTER(CostCase),
+                                        ctypes.POINTER(Cost)]
     lib.mla_last_error.restype = ctypes.c_char_p
     lib.mla_last_error.argtypes = []
     lib.mla_version.restype = ctypes.c_int32
@@ -196,6 +227,21 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
     _check(lib, fn(*args))
     return result
+
+
+def primitive_costs(mq, chunk_tokens, q_bytes=1152, p_bytes=1032, kv_bytes=1152, **model):
+    """ROUTE / FETCH / LOCAL costs of one (chunk, request) case from the
+    closed-form model (host arithmetic in the library).  `model` overrides
+    fields of PAPER_COST_MODEL.  Returns a dict of the mla_cost_t fields,
+    with `choice` as a primitive name."""
+    lib = load()
+    m = CostModel(**{**PAPER_COST_MODEL, **model})
+    c = CostCase(mq, chunk_tokens, q_bytes, p_bytes, kv_bytes)
+    out = Cost()
+    _check(lib, lib.mla_primitive_costs(ctypes.byref(m), ctypes.byref(c), ctypes.byref(out)))
+    res = {f: getattr(out, f) for f, _ in Cost._fields_ if f != "reserved"}
+    res["choice"] = PRIMITIVES[res["choice"]]
+    return res
 
 
 def _merge_args(parts_lat, parts_lse, out, out_lse, stream):
