@@ -40,7 +40,9 @@ def parse():
     ap.add_argument("--workload", default="batched-merge",
                     help="batched-merge | dsv3-one-request | few-head | dense-local | "
                          "dense-local-fp8 | tiny | holder-{dense|sparse}-n<N>-h<H>[-jobs] "
-                         "(one holder chunk serving N requesters)")
+                         "(one holder chunk serving N requesters) | "
+                         "select-{tok|blk|dense}-b<B>-k<k>-c<corpus>[-h<H>] (selection budget) | "
+                         "fetch-splice-c<n>-l<L> | fetch-gather-k<k>-c<corpus>-l<L> (FETCH side)")
     ap.add_argument("--n-splits", type=int, default=0, help="split-K override (0 = library)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 = skip)")
@@ -78,12 +80,99 @@ def algorithmic(w):
     return flops, kv + q + out, kv
 
 
+def bench_fetch(args):
+    """The FETCH-side kernels: the splice of a pulled chunk (every layer, one
+    launch) or the gather of a selected token set.  One step = one call."""
+    import torch
+    from paper_2606_01502_amd import mla, workloads as W
+    from tests import gpu_helpers as G
+
+    mla.load()
+    w = W.fetch_inputs(args.workload)
+    dev = G.device()
+
+    def bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    stream = torch.cuda.Stream()
+    ckv, kpe, table = bf16(w["ckv"]), bf16(w["kpe"]), i32(w["table"])
+    L, n = w["L"], w["n"]
+    if w["kind"] == "splice":
+        cc, ck = bf16(w["chunk_ckv"]), bf16(w["chunk_kpe"])
+
+        def call():
+            mla.fetch_splice(cc, ck, ckv, kpe, table, w["dst_start"], w["delta"], stream=stream)
+    else:
+        sel = i32(w["sel"])
+        oc = torch.empty((L, n, DLAT), dtype=torch.bfloat16, device=dev)
+        ok = torch.empty((L, n, DPE), dtype=torch.bfloat16, device=dev)
+
+        def call():
+            mla.fetch_gather(ckv, kpe, table, sel, oc, ok, stream=stream)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            call()
+        stream.synchronize()
+        t_w = time.perf_counter()
+        while time.perf_counter() - t_w < args.warmup_seconds:
+            call()
+            stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            call()
+        e1.record(stream)
+        stream.synchronize()
+        t1 = time.perf_counter()
+    ms = e0.elapsed_time(e1) / args.steps
+    # algorithmic bytes: every token row read once and written once, all layers
+    alg_bytes = 2 * L * n * (DLAT + DPE) * 2
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    cpu = None
+    if args.cpu_seconds > 0:
+        # the oracle on one layer of the same call, scaled to all L layers
+        from oracle import fetch as F  # test infrastructure: the CPU baseline only
+        ts = time.perf_counter()
+        if w["kind"] == "splice":
+            F.splice(w["chunk_ckv"][:1], w["chunk_kpe"][:1], w["ckv"][:1], w["kpe"][:1],
+                     w["table"], w["dst_start"], w["delta"], 10000.0, 0)
+        else:
+            F.gather(w["ckv"][:1], w["kpe"][:1], w["table"], w["sel"])
+        one = time.perf_counter() - ts
+        cpu = {"value": one * L * 1e6, "unit": "us/call", "cores": 1, "kind": "oracle",
+               "sample": f"1 of {L} layers, numpy oracle, scaled by {L}"}
+    what = "splice of a pulled chunk" if w["kind"] == "splice" else "gather of a selected set"
+    res = {
+        "metric": f"us per FETCH {what} (all layers, one call)",
+        "value": ms * 1e3, "unit": "us/call", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w["name"], "layers": L, "tokens": n},
+        "host_wall_ms_per_step": (t1 - t0) * 1e3 / args.steps,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "splice_kernel" if w["kind"] == "splice" else "gather_kernel",
+                     "algorithmic_bytes": alg_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
+    if args.workload.startswith("fetch-"):
+        return bench_fetch(args)
 
     import torch
     from paper_2606_01502_amd import mla, workloads as W

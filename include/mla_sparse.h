@@ -217,6 +217,51 @@ const char* mla_last_error(void);
 int32_t mla_version(void);
 
 /*
+ * FETCH-side copies on one GPU (Section 2.2): what the move-the-cache
+ * primitive does with the latent cache instead of routing the query.  Both
+ * run every layer of a chunk in one launch.  Pools hold L layers,
+ * [L, P, 64, 512] and [L, P, 64, 64] bf16, contiguous, 16-byte aligned.
+ *
+ * mla_fetch_gather: the scattered gather of a selected token set into a
+ * contiguous payload (FETCH's residual work under sparse selection).
+ *   chunk_block_table [NB] int32    logical block of the chunk -> pool block
+ *   sel_token_ids     [K]  int32    logical tokens (block * 64 + t); -1 = empty
+ *   out_ckv [L, K, 512], out_kpe [L, K, 64] bf16, written: entry j is pool
+ *                                   token table[s / 64] * 64 + s % 64 of slot
+ *                                   j's id s, copied bit for bit; an empty
+ *                                   slot, an id outside [0, 64 NB) or a table
+ *                                   entry outside [0, P) gives a zero row
+ */
+mla_status_t mla_fetch_gather(const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                              const mla_tensor_t* chunk_block_table,
+                              const mla_tensor_t* sel_token_ids, const mla_tensor_t* out_ckv,
+                              const mla_tensor_t* out_kpe, void* stream);
+
+/* mla_fetch_splice: scatter a pulled chunk into the requester's paged pools,
+ * re-homed at a new position.
+ *   chunk_ckv [L, n, 512], chunk_kpe [L, n, 64] bf16   the chunk, token t
+ *   ckv_pool, kpe_pool                                 written in place
+ *   block_table [NB] int32    the requester's logical blocks -> pool blocks
+ *   dst_start                 position of token 0 in the requester's
+ *                             sequence: token t goes to row (dst_start + t)
+ *                             % 64 of block block_table[(dst_start + t) / 64];
+ *                             dst_start + n <= 64 NB
+ *   delta                     positions the chunk moves (new - old start)
+ *   rope_base, pairing        the RoPE layout (a reading; the paper gives
+ *                             none): pair i turns at rope_base^(-2i/64);
+ *                             pairing 0 pairs dims (2i, 2i+1), 1 pairs
+ *                             (i, i+32)
+ * The latent row is copied bit for bit; each RoPE pair (x, y) becomes
+ * (x cos a - y sin a, x sin a + y cos a), a = delta * rope_base^(-2i/64)
+ * (cos and sin in double on the host, the products in fp32, one rounding
+ * to bf16).  A token whose table entry is outside [0, P) is skipped; no
+ * other pool row is touched. */
+mla_status_t mla_fetch_splice(const mla_tensor_t* chunk_ckv, const mla_tensor_t* chunk_kpe,
+                              const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                              const mla_tensor_t* block_table, int64_t dst_start, int64_t delta,
+                              float rope_base, int32_t pairing, void* stream);
+
+/*
  * The closed-form cost model of the three redistribution primitives and the
  * selection predicate (Sections 4.1-4.2 and 5.1-5.2).  Host-only arithmetic:
  * no device, no stream; a scheduler evaluates it per (chunk, request).

@@ -67,18 +67,22 @@ def rotate(kpe_f64, delta, base, pairing):
 
 
 def gather(ckv_pool, kpe_pool, table, sel):
-    """Contiguous copy of the selected tokens: for every slot j with
-    s = sel[j] >= 0, entry j holds token s % 64 of pool block
-    table[s // 64], for each layer.  Pools [L, P, 64, D], table [NB],
-    sel [K]; returns (ckv [L, n, 512], kpe [L, n, 64]) with n the valid
-    slots, in slot order."""
-    L = ckv_pool.shape[0]
-    valid = [int(s) for s in sel if s >= 0]
-    out_c = np.empty((L, len(valid), DLAT), ckv_pool.dtype)
-    out_k = np.empty((L, len(valid), DPE), kpe_pool.dtype)
-    for layer in range(L):
-        for j, s in enumerate(valid):
-            b, t = int(table[s // BLOCK]), s % BLOCK
+    """Copy of the selected tokens in slot order: for every slot j with
+    s = sel[j], entry j holds token s % 64 of pool block table[s // 64],
+    for each layer; an empty slot (-1), an id outside [0, 64 NB) or a table
+    entry outside [0, P) gives a zero row.  Pools [L, P, 64, D], table
+    [NB], sel [K]; returns (ckv [L, K, 512], kpe [L, K, 64])."""
+    L, P = ckv_pool.shape[:2]
+    K = len(sel)
+    out_c = np.zeros((L, K, DLAT), ckv_pool.dtype)
+    out_k = np.zeros((L, K, DPE), kpe_pool.dtype)
+    for j, s in enumerate(int(v) for v in sel):
+        if s < 0 or s >= len(table) * BLOCK:
+            continue
+        b, t = int(table[s // BLOCK]), s % BLOCK
+        if not 0 <= b < P:
+            continue
+        for layer in range(L):
             out_c[layer, j] = ckv_pool[layer, b, t]
             out_k[layer, j] = kpe_pool[layer, b, t]
     return out_c, out_k

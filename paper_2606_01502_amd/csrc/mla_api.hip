@@ -81,6 +81,20 @@ mla_status_t check_tensor(const mla_tensor_t* t, const char* name, int32_t dtype
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Row-major contiguous with the given shape.
+bool contiguous(const mla_tensor_t& t, std::initializer_list<int64_t> shape) {
+  if (t.ndim != (int)shape.size()) return false;
+  int d = 0;
+  for (int64_t v : shape)
+    if (t.shape[d++] != v) return false;
+  int64_t st = 1;
+  for (int k = t.ndim - 1; k >= 0; --k) {
+    if (t.shape[k] > 1 && t.stride[k] != st) return false;
+    st *= t.shape[k];
+  }
+  return true;
+}
+
 // Rows of a [.., .., .., D] tensor are 16-byte aligned: base and every outer stride.
 bool rows_aligned(const mla_tensor_t& t, int es) {
   if (!aligned16(t.data)) return false;
@@ -426,6 +440,118 @@ mla_status_t mla_primitive_costs(const mla_cost_model_t* m, const mla_cost_case_
   r.splice_crossover_tokens = m->prefill_us > 0.0 ? m->splice_us / (L * m->prefill_us) : INFINITY;
   *out = r;
   return MLA_OK;
+}
+
+mla_status_t mla_fetch_gather(const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                              const mla_tensor_t* chunk_block_table,
+                              const mla_tensor_t* sel_token_ids, const mla_tensor_t* out_ckv,
+                              const mla_tensor_t* out_kpe, void* stream) {
+  try {
+    g_last_error.clear();
+    mla_status_t st;
+    if ((st = check_tensor(ckv_pool, "ckv_pool", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(kpe_pool, "kpe_pool", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(chunk_block_table, "chunk_block_table", MLA_DTYPE_INT32, 1)) != MLA_OK) return st;
+    if ((st = check_tensor(sel_token_ids, "sel_token_ids", MLA_DTYPE_INT32, 1)) != MLA_OK) return st;
+    if ((st = check_tensor(out_ckv, "out_ckv", MLA_DTYPE_BF16, 3)) != MLA_OK) return st;
+    if ((st = check_tensor(out_kpe, "out_kpe", MLA_DTYPE_BF16, 3)) != MLA_OK) return st;
+    const int64_t L = ckv_pool->shape[0], P = ckv_pool->shape[1];
+    const int64_t NB = chunk_block_table->shape[0], K = sel_token_ids->shape[0];
+    if (!contiguous(*ckv_pool, {L, P, MLA_BLOCK, MLA_DLAT}) || !contiguous(*kpe_pool, {L, P, MLA_BLOCK, MLA_DPE}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be contiguous [L, P, 64, 512] and [L, P, 64, 64]");
+    if (!contiguous(*chunk_block_table, {NB}) || !contiguous(*sel_token_ids, {K}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_block_table and sel_token_ids must be contiguous");
+    if (!contiguous(*out_ckv, {L, K, MLA_DLAT}) || !contiguous(*out_kpe, {L, K, MLA_DPE}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "out_ckv / out_kpe must be contiguous [L, K, 512] / [L, K, 64]");
+    if (!aligned16(ckv_pool->data) || !aligned16(kpe_pool->data) || !aligned16(out_ckv->data) ||
+        !aligned16(out_kpe->data))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "pools and outputs must be 16-byte aligned");
+    if (NB > (INT32_MAX >> 6) || P > INT32_MAX || L * ((K + 63) / 64) > INT32_MAX)
+      return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the index range");
+    const Extent outs[2] = {extent(*out_ckv), extent(*out_kpe)};
+    const Extent ins[4] = {extent(*ckv_pool), extent(*kpe_pool), extent(*chunk_block_table),
+                           extent(*sel_token_ids)};
+    if (overlaps(outs[0], outs[1])) return fail(MLA_ERR_INVALID_ARGUMENT, "out_ckv and out_kpe overlap");
+    for (const Extent& o : outs)
+      for (const Extent& i : ins)
+        if (overlaps(o, i)) return fail(MLA_ERR_INVALID_ARGUMENT, "an output overlaps an input");
+    mla::FetchParams p{};
+    p.src_ckv = (const uint16_t*)ckv_pool->data;
+    p.src_kpe = (const uint16_t*)kpe_pool->data;
+    p.dst_ckv = (uint16_t*)out_ckv->data;
+    p.dst_kpe = (uint16_t*)out_kpe->data;
+    p.table = (const int32_t*)chunk_block_table->data;
+    p.sel = (const int32_t*)sel_token_ids->data;
+    p.P = P;
+    p.n = K;
+    p.n_ids = NB * MLA_BLOCK;
+    p.L = (int32_t)L;
+    hipError_t e = mla::launch_fetch_gather(p, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("gather kernel launch: ") + hipGetErrorString(e));
+    return MLA_OK;
+  } catch (...) {
+    return fail(MLA_ERR_HIP, "internal error");
+  }
+}
+
+mla_status_t mla_fetch_splice(const mla_tensor_t* chunk_ckv, const mla_tensor_t* chunk_kpe,
+                              const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
+                              const mla_tensor_t* block_table, int64_t dst_start, int64_t delta,
+                              float rope_base, int32_t pairing, void* stream) {
+  try {
+    g_last_error.clear();
+    mla_status_t st;
+    if ((st = check_tensor(chunk_ckv, "chunk_ckv", MLA_DTYPE_BF16, 3)) != MLA_OK) return st;
+    if ((st = check_tensor(chunk_kpe, "chunk_kpe", MLA_DTYPE_BF16, 3)) != MLA_OK) return st;
+    if ((st = check_tensor(ckv_pool, "ckv_pool", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(kpe_pool, "kpe_pool", MLA_DTYPE_BF16, 4)) != MLA_OK) return st;
+    if ((st = check_tensor(block_table, "block_table", MLA_DTYPE_INT32, 1)) != MLA_OK) return st;
+    const int64_t L = chunk_ckv->shape[0], n = chunk_ckv->shape[1];
+    const int64_t P = ckv_pool->shape[1], NB = block_table->shape[0];
+    if (!contiguous(*chunk_ckv, {L, n, MLA_DLAT}) || !contiguous(*chunk_kpe, {L, n, MLA_DPE}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_ckv / chunk_kpe must be contiguous [L, n, 512] / [L, n, 64]");
+    if (!contiguous(*ckv_pool, {L, P, MLA_BLOCK, MLA_DLAT}) || !contiguous(*kpe_pool, {L, P, MLA_BLOCK, MLA_DPE}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be contiguous [L, P, 64, 512] and [L, P, 64, 64] with the chunk's L");
+    if (!contiguous(*block_table, {NB})) return fail(MLA_ERR_INVALID_ARGUMENT, "block_table must be contiguous");
+    if (!aligned16(chunk_ckv->data) || !aligned16(chunk_kpe->data) || !aligned16(ckv_pool->data) ||
+        !aligned16(kpe_pool->data))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "chunk and pools must be 16-byte aligned");
+    if (pairing != 0 && pairing != 1) return fail(MLA_ERR_INVALID_ARGUMENT, "pairing must be 0 or 1");
+    if (!(rope_base > 0.f) || !std::isfinite(rope_base))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "rope_base must be finite and > 0");
+    if (dst_start < 0 || dst_start > NB * MLA_BLOCK - n)
+      return fail(MLA_ERR_INVALID_ARGUMENT, "the chunk must fit the block table: 0 <= dst_start, dst_start + n <= 64 NB");
+    if (P > INT32_MAX || L * ((n + 63) / 64) > INT32_MAX)
+      return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the index range");
+    const Extent outs[2] = {extent(*ckv_pool), extent(*kpe_pool)};
+    const Extent ins[3] = {extent(*chunk_ckv), extent(*chunk_kpe), extent(*block_table)};
+    if (overlaps(outs[0], outs[1])) return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool and kpe_pool overlap");
+    for (const Extent& o : outs)
+      for (const Extent& i : ins)
+        if (overlaps(o, i)) return fail(MLA_ERR_INVALID_ARGUMENT, "a pool overlaps the chunk or the table");
+    mla::FetchParams p{};
+    p.src_ckv = (const uint16_t*)chunk_ckv->data;
+    p.src_kpe = (const uint16_t*)chunk_kpe->data;
+    p.dst_ckv = (uint16_t*)ckv_pool->data;
+    p.dst_kpe = (uint16_t*)kpe_pool->data;
+    p.table = (const int32_t*)block_table->data;
+    p.P = P;
+    p.n = n;
+    p.dst_start = dst_start;
+    p.L = (int32_t)L;
+    p.pairing = pairing;
+    // pair i turns through delta * base^(-2i/64), evaluated in double
+    for (int i = 0; i < MLA_DPE / 2; ++i) {
+      const double ang = (double)delta * std::pow((double)rope_base, -2.0 * i / MLA_DPE);
+      p.cs[i] = (float)std::cos(ang);
+      p.sn[i] = (float)std::sin(ang);
+    }
+    hipError_t e = mla::launch_fetch_splice(p, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("splice kernel launch: ") + hipGetErrorString(e));
+    return MLA_OK;
+  } catch (...) {
+    return fail(MLA_ERR_HIP, "internal error");
+  }
 }
 
 mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,

@@ -71,6 +71,27 @@ struct MergeParams {
   int64_t ol_s0, ol_s1, ol_s2;
 };
 
+// FETCH-side copy kernels: one workgroup moves 64 tokens of one layer.
+struct FetchParams {
+  // splice: chunk rows [L][n][D] -> pool rows; gather: pool rows -> out rows [L][K][D]
+  const uint16_t* src_ckv;
+  const uint16_t* src_kpe;
+  uint16_t* dst_ckv;
+  uint16_t* dst_kpe;
+  const int32_t* table;  // logical block -> pool block
+  const int32_t* sel;    // gather: selected logical tokens [K], -1 = empty
+  int64_t P;             // pool blocks per layer
+  int64_t n;             // tokens per layer: chunk tokens (splice) or slots K (gather)
+  int64_t n_ids;         // gather: 64 * NB (logical tokens of the chunk)
+  int64_t dst_start;     // splice: position of the chunk's first token in the requester's sequence
+  int32_t L;
+  int32_t pairing;       // 0: dims (2i, 2i+1); 1: dims (i, i + 32)
+  float cs[32], sn[32];  // splice: cos, sin of delta * theta_i
+};
+
+hipError_t launch_fetch_gather(const FetchParams& p, hipStream_t s);
+hipError_t launch_fetch_splice(const FetchParams& p, hipStream_t s);
+
 // Cache kinds of the partial kernel.
 constexpr int kKvBf16 = 0;
 constexpr int kKvFp8Shared = 1;  // e4m3, one scale per block for ckv and kpe

@@ -27,7 +27,8 @@ DTYPE_BF16, DTYPE_FP8_E4M3FN, DTYPE_FP32, DTYPE_INT32 = 1, 2, 3, 4
 
 EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex",
            "mla_sparse_partial_attn_tokens", "mla_merge_partials", "mla_merge_partials_ex",
-           "mla_last_error", "mla_version", "mla_primitive_costs")
+           "mla_last_error", "mla_version", "mla_primitive_costs", "mla_fetch_gather",
+           "mla_fetch_splice")
 
 
 class MlaError(RuntimeError):
@@ -100,6 +101,11 @@ def load(path: str = LIB_PATH):
     lib.mla_merge_partials.argtypes = [PP, PP, ctypes.c_int32, P, vp]
     lib.mla_merge_partials_ex.restype = ctypes.c_int
     lib.mla_merge_partials_ex.argtypes = [PP, PP, ctypes.c_int32, P, P, vp]
+    lib.mla_fetch_gather.restype = ctypes.c_int
+    lib.mla_fetch_gather.argtypes = [P, P, P, P, P, P, vp]
+    lib.mla_fetch_splice.restype = ctypes.c_int
+    lib.mla_fetch_splice.argtypes = [P, P, P, P, P, ctypes.c_int64, ctypes.c_int64,
+                                     ctypes.c_float, ctypes.c_int32, vp]
     lib.mla_primitive_costs.restype = ctypes.c_int
     lib.mla_primitive_costs.argtypes = [ctypes.POINTER(CostModel), ctypes.POINTER(CostCase),
                                         ctypes.POINTER(Cost)]
@@ -227,6 +233,36 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
     _check(lib, fn(*args))
     return result
+
+
+def fetch_gather(ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, out_ckv=None,
+                 out_kpe=None, stream=None):
+    """FETCH's scattered gather: the selected tokens of every layer, in slot
+    order, as contiguous bf16 [L, K, 512] / [L, K, 64] (zero rows for empty
+    slots).  Pools are [L, P, 64, 512] / [L, P, 64, 64] bf16."""
+    L = ckv_pool.shape[0]
+    K = sel_token_ids.shape[0]
+    if out_ckv is None:
+        out_ckv = torch.empty((L, K, DLAT), dtype=torch.bfloat16, device=ckv_pool.device)
+    if out_kpe is None:
+        out_kpe = torch.empty((L, K, DPE), dtype=torch.bfloat16, device=ckv_pool.device)
+    lib = load()
+    d = [describe(t) for t in (ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, out_ckv,
+                               out_kpe)]
+    _check(lib, lib.mla_fetch_gather(*[_ref(x) for x in d], _stream(stream)))
+    return out_ckv, out_kpe
+
+
+def fetch_splice(chunk_ckv, chunk_kpe, ckv_pool, kpe_pool, block_table, dst_start, delta,
+                 rope_base=10000.0, pairing=0, stream=None):
+    """FETCH's splice: write the chunk [L, n, 512] / [L, n, 64] into the
+    paged pools at positions dst_start .. dst_start + n - 1 of the sequence
+    that block_table maps, its RoPE pairs turned by delta positions
+    (pairing 0: dims (2i, 2i+1), 1: dims (i, i+32))."""
+    lib = load()
+    d = [describe(t) for t in (chunk_ckv, chunk_kpe, ckv_pool, kpe_pool, block_table)]
+    _check(lib, lib.mla_fetch_splice(*[_ref(x) for x in d], int(dst_start), int(delta),
+                                     float(rope_base), int(pairing), _stream(stream)))
 
 
 def primitive_costs(mq, chunk_tokens, q_bytes=1152, p_bytes=1032, kv_bytes=1152, **model):

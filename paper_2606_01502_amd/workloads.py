@@ -372,6 +372,39 @@ def selection(kind, n_req, k, corpus, heads=128, seed=8):
                     n_requests=n_req, merge_parts=1, tokens=kind == "tok")
 
 
+def fetch_inputs(name, seed=9):
+    """FETCH-side workloads (Section 2.2), as a dict of host arrays:
+      fetch-splice-c<n>-l<L>: a pulled chunk of n tokens x L layers (~ N(0,
+        0.5), bf16) to splice into a requester's paged pools of 2n + 128
+        tokens per layer, re-homed at position 37 (not block aligned) with
+        the chunk moving by delta = 4096 positions;
+      fetch-gather-k<k>-c<c>-l<L>: k tokens drawn uniformly without
+        replacement over a c-token chunk of L layers, gathered into a
+        contiguous payload.
+    The paper's case is c = 2048 tokens of a 27-layer model."""
+    parts = name.split("-")
+    kind = parts[1]
+    rng = np.random.default_rng([seed, _T_SEL])
+    if kind == "splice":
+        n, L = int(parts[2][1:]), int(parts[3][1:])
+        nb = (2 * n + 127) // BLOCK + 2
+        P = nb + 3
+        chunk_ckv = normal_bf16(seed, _T_CKV, (L, n, DLAT), 0.5)
+        chunk_kpe = normal_bf16(seed, _T_KPE, (L, n, DPE), 0.5)
+        ckv = normal_bf16(seed + 1, _T_CKV, (L, P, BLOCK, DLAT), 0.5)
+        kpe = normal_bf16(seed + 1, _T_KPE, (L, P, BLOCK, DPE), 0.5)
+        table = _perm(seed, P)[:nb].astype(np.int32)
+        return dict(kind=kind, name=name, chunk_ckv=chunk_ckv, chunk_kpe=chunk_kpe, ckv=ckv,
+                    kpe=kpe, table=table, dst_start=37, delta=4096, n=n, L=L)
+    k, c, L = int(parts[2][1:]), int(parts[3][1:]), int(parts[4][1:])
+    nb = c // BLOCK
+    ckv = normal_bf16(seed, _T_CKV, (L, nb, BLOCK, DLAT), 0.5)
+    kpe = normal_bf16(seed, _T_KPE, (L, nb, BLOCK, DPE), 0.5)
+    table = _perm(seed, nb).astype(np.int32)
+    sel = np.sort(rng.choice(c, k, replace=False)).astype(np.int32)
+    return dict(kind=kind, name=name, ckv=ckv, kpe=kpe, table=table, sel=sel, n=k, L=L)
+
+
 CONFIGS = {
     "tiny": tiny,
     "dsv3-one-request": dsv3_one_request,

@@ -35,11 +35,12 @@ def test_gather_whole_chunk_is_its_blocks():
     gc, gk = F.gather(ckv, kpe, table, sel)
     assert np.array_equal(gc, ckv[:, table].reshape(2, -1, 512))
     assert np.array_equal(gk, kpe[:, table].reshape(2, -1, 64))
-    # empty slots are skipped, order is slot order, duplicates repeat
-    sel2 = np.array([130, -1, 5, 130], np.int32)
+    # slot order, duplicates repeat, empty and out-of-range slots are zero rows
+    sel2 = np.array([130, -1, 5, 130, 3 * 64], np.int32)
     gc2, _ = F.gather(ckv, kpe, table, sel2)
     seq = ckv[:, table].reshape(2, -1, 512)
-    assert np.array_equal(gc2, seq[:, [130, 5, 130]])
+    assert np.array_equal(gc2[:, [0, 2, 3]], seq[:, [130, 5, 130]])
+    assert not gc2[:, [1, 4]].any()
 
 
 def test_splice_placement_and_identity():
