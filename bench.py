@@ -54,12 +54,12 @@ def parse():
     return ap.parse_args()
 
 
-def counted_traffic(workload, n_splits):
-    """HBM bytes per launch of the partial kernel from the committed rocprofv3
+def counted_traffic(workload, n_splits, kernel="partial_kernel"):
+    """HBM bytes per launch of the kernel from the committed rocprofv3
     counter summary (FETCH_SIZE / WRITE_SIZE scaled by a known-size copy), or
     None when that summary is for another workload or an older kernel source."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"partial_kernel_{workload}_counters.json")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.json")
     if n_splits != 0 or not os.path.exists(path):
         return None
     with open(path) as f:
@@ -121,6 +121,12 @@ def bench_fetch(args):
         while time.perf_counter() - t_w < args.warmup_seconds:
             call()
             stream.synchronize()
+        if args.copy_calibration_mib > 0:
+            src = torch.ones(args.copy_calibration_mib << 18, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            stream.synchronize()
+            del src, dst
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -149,6 +155,7 @@ def bench_fetch(args):
         cpu = {"value": one * L * 1e6, "unit": "us/call", "cores": 1, "kind": "oracle",
                "sample": f"1 of {L} layers, numpy oracle, scaled by {L}"}
     what = "splice of a pulled chunk" if w["kind"] == "splice" else "gather of a selected set"
+    kernel = "splice_kernel" if w["kind"] == "splice" else "gather_kernel"
     res = {
         "metric": f"us per FETCH {what} (all layers, one call)",
         "value": ms * 1e3, "unit": "us/call", "n_gpus": 1, "steps": args.steps,
@@ -157,8 +164,8 @@ def bench_fetch(args):
         "config": {"workload": w["name"], "layers": L, "tokens": n},
         "host_wall_ms_per_step": (t1 - t0) * 1e3 / args.steps,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "splice_kernel" if w["kind"] == "splice" else "gather_kernel",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": counted_traffic(w["name"], 0, kernel), "kernel": kernel,
                      "algorithmic_bytes": alg_bytes},
         "cpu_baseline": cpu,
     }
