@@ -204,8 +204,6 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K] or [R, Mq, K]");
     if (per_row && fp8)
       return fail(MLA_ERR_UNSUPPORTED, "per-row selections need a bf16 cache");
-    if (tokens && fp8)
-      return fail(MLA_ERR_UNSUPPORTED, "token selections need a bf16 cache");
     if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
     if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
     if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||

@@ -268,6 +268,16 @@ __device__ __forceinline__ void scale_inplace(f32x4_t& x, float s) {
   x = f32x4_t{x0, x1, x2, x3};
 }
 
+// x[i] *= s[i] in the registers x already occupies.
+__device__ __forceinline__ void scale_inplace4(f32x4_t& x, f32x4_t s) {
+  float x0 = x[0], x1 = x[1], x2 = x[2], x3 = x[3];
+  asm volatile("v_mul_f32 %0, %0, %4\n\tv_mul_f32 %1, %1, %5\n\tv_mul_f32 %2, %2, %6\n\t"
+               "v_mul_f32 %3, %3, %7"
+               : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3)
+               : "v"(s[0]), "v"(s[1]), "v"(s[2]), "v"(s[3]));
+  x = f32x4_t{x0, x1, x2, x3};
+}
+
 __device__ __forceinline__ float xor_max(float v) {
   v = fmaxf(v, __shfl_xor(v, 16));
   return fmaxf(v, __shfl_xor(v, 32));
@@ -429,6 +439,36 @@ struct TokIssue {
       asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                    :: "v"(a), "s"(d) : "memory", "m0");
     }
+  }
+};
+
+// The fp8 loads of a virtual block of 64 listed tokens, into the same stage
+// layout as a pool block (see issue_load): latent load j < 8 of wave w holds
+// the stage's tokens 16w + 2j and 16w + 2j + 1 (lanes 0-31 and 32-63), load
+// 8 the RoPE rows of tokens 16w .. 16w+15; every lane has its own address.
+struct TokIssue8 {
+  int tok;       // pool token of stage token 16w + (lane & 15)
+  uint32_t buf;  // LDS address of the stage
+  __device__ __forceinline__ void load(const PartialParams& p, int j, int wave, int lane_in) const {
+    int lane;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(lane) : "v"(lane_in));
+    const uint8_t* a;
+    uint32_t d;
+    if (j < 8) {
+      const int src = 2 * j + (lane >> 5);
+      const int t = 16 * wave + src;
+      const uint32_t c = (uint32_t)((lane & 31) ^ fp8_key(t));
+      a = p.ckv + (uint64_t)(uint32_t)__shfl(tok, src) * 512u + (c << 4);
+      d = buf + (uint32_t)(8 * wave + j) * 1024u;
+    } else {
+      const int src = lane >> 2;
+      const int t = 16 * wave + src;
+      const uint32_t c = (uint32_t)((lane & 3) ^ fp8_rope_key(t));
+      a = p.kpe + (uint64_t)(uint32_t)__shfl(tok, src) * 64u + (c << 4);
+      d = buf + (uint32_t)Layout<true>::kStageCkv + (uint32_t)wave * 1024u;
+    }
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(a), "s"(__builtin_amdgcn_readfirstlane(d)) : "memory", "m0");
   }
 };
 
@@ -630,11 +670,15 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
 // nslots) of job r into the LDS list as pool tokens (table[r, id / 64] * 64 +
 // id % 64), slot order kept, and fill the list up to the next multiple of 64
 // with the first entry, so that the last virtual block loads only listed
-// tokens (the fill is masked out of the softmax).  Returns the number of
-// listed tokens.
+// tokens (the fill is masked out of the softmax).  fp8: entry i's latent
+// scale goes to tok_scales[i] and its RoPE / latent scale ratio to
+// tok_scales[kMaxSlotsPerSplit + i] (each token carries its own block's
+// scales).  Returns the number of listed tokens.
+template <bool FP8>
 __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int slot0,
                                               int nslots, LDS uint8_t* smem, int tid) {
-  using L = Layout<false>;
+  using L = Layout<FP8>;
+  LDS float* tok_scales = (LDS float*)(smem + L::kScales);
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   LDS int* list = (LDS int*)(smem + L::kList);
@@ -662,14 +706,28 @@ __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int
       off += (w < wave) ? c : 0;
       total += c;
     }
-    if (pt >= 0) list[off + before] = pt;
+    if (pt >= 0) {
+      list[off + before] = pt;
+      if constexpr (FP8) {
+        const int bb = pt >> 6;
+        const float sc = p.ckv_scale[bb];
+        tok_scales[off + before] = sc;
+        tok_scales[kMaxSlotsPerSplit + off + before] = p.kpe_scale[bb] / sc;
+      }
+    }
     n_tok += total;
     lds_barrier();
   }
   const int padded = (n_tok + kBlock - 1) & ~(kBlock - 1);
-  if (tid >= n_tok && tid < padded) list[tid] = list[0];
-  for (int i = tid + 256; i < padded; i += 256)
-    if (i >= n_tok) list[i] = list[0];
+  for (int i = tid; i < padded; i += 256) {
+    if (i >= n_tok) {
+      list[i] = list[0];
+      if constexpr (FP8) {
+        tok_scales[i] = tok_scales[0];
+        tok_scales[kMaxSlotsPerSplit + i] = tok_scales[kMaxSlotsPerSplit];
+      }
+    }
+  }
   lds_barrier();
   return n_tok;
 }
@@ -684,7 +742,7 @@ void partial_kernel(const PartialParams p) {
   constexpr bool FP8 = KV != kKvBf16;
   constexpr bool PR = SEL == kSelPerRow;   // a block selection per query row
   constexpr bool TOK = SEL == kSelTokens;  // token selections, 64 to a virtual block
-  static_assert(!((PR || TOK) && FP8), "per-row and token selections: bf16 caches only");
+  static_assert(!(PR && FP8), "per-row selections: bf16 caches only");
   constexpr bool kSplitScales = KV == kKvFp8Split;
   using L = Layout<FP8>;
   constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
@@ -725,7 +783,7 @@ void partial_kernel(const PartialParams p) {
                   ? compact_per_row(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
                   : compact_per_row(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
   } else if constexpr (TOK) {
-    n_tok = compact_tokens(p, r, slot0, nslots, smem, tid);
+    n_tok = compact_tokens<FP8>(p, r, slot0, nslots, smem, tid);
     n_valid = (n_tok + kBlock - 1) / kBlock;
   } else {
     n_valid = compact_slots<FP8>(p, r, slot0, nslots, smem, tid);
@@ -733,8 +791,16 @@ void partial_kernel(const PartialParams p) {
 
   // ---- the first blocks' loads go out before the query rows, so that their
   // latencies overlap
-  if constexpr (TOK) {
-    static_assert(L::kLead == 1, "token selections stream one virtual block ahead");
+  if constexpr (TOK && FP8) {
+    for (int h = 0; h < n_valid && h < L::kLead; ++h) {
+      TokIssue8 ti;
+      ti.tok = list[h * kBlock + 16 * wave + (lane & 15)];
+      ti.buf = (uint32_t)(uintptr_t)(stage0 + h * L::kStage);
+#pragma unroll
+      for (int j = 0; j < L::kLoads; ++j) ti.load(p, j, wave, lane);
+    }
+  } else if constexpr (TOK) {
+    static_assert(L::kLead == 1, "bf16 token selections stream one virtual block ahead");
     if (n_valid > 0) {
       TokIssue ti;
       ti.tok = list[16 * wave + (lane & 15)];
@@ -817,7 +883,7 @@ void partial_kernel(const PartialParams p) {
     // the softmax scale times the latent scale; P is scaled by the latent
     // scale before its bf16 rounding.
     float s_mult = p.scale_log2, v_mult = 1.f, pe_ratio = 1.f;
-    if constexpr (FP8) {
+    if constexpr (FP8 && !TOK) {
       v_mult = scales[2 * h];
       if constexpr (kSplitScales) pe_ratio = scales[2 * h + 1];
       s_mult = p.scale_log2 * v_mult;
@@ -830,7 +896,7 @@ void partial_kernel(const PartialParams p) {
     // fp8 (9 loads): all at once after the first key reads.
     LDS uint8_t* const next_buf = stage0 + (hn % L::kNum) * L::kStage;
     typename std::conditional<TOK, TokIssue, Bf16Issue>::type bi;
-    if constexpr (TOK) {
+    if constexpr (TOK && !FP8) {
       bi.tok = b_next >= 0 ? list[hn * kBlock + 16 * wave + (lane & 15)] : 0;
       bi.m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + (uint32_t)wave * 16384u);
       bi.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + 65536u + (uint32_t)wave * 2048u);
@@ -842,7 +908,17 @@ void partial_kernel(const PartialParams p) {
       bi.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + 65536u + (uint32_t)wave * 2048u);
     }
     auto issue_next = [&]() {
-      if (b_next >= 0) issue_stage<FP8>(p, b_next, next_buf, wave, lane);
+      if constexpr (TOK) {
+        if (b_next >= 0) {
+          TokIssue8 ti;
+          ti.tok = list[hn * kBlock + 16 * wave + (lane & 15)];
+          ti.buf = (uint32_t)(uintptr_t)next_buf;
+#pragma unroll
+          for (int j = 0; j < L::kLoads; ++j) ti.load(p, j, wave, lane);
+        }
+      } else {
+        if (b_next >= 0) issue_stage<FP8>(p, b_next, next_buf, wave, lane);
+      }
       __builtin_amdgcn_sched_barrier(0);
     };
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
@@ -850,6 +926,17 @@ void partial_kernel(const PartialParams p) {
     // the loop.
     const int ln = lds_opaque(lane);
     const int ln16 = ln & 15, lg = ln >> 4;
+    // fp8 token selections: the RoPE / latent ratios of the lane's tokens
+    // 16 tau + 4 lg + k (its S^T accumulator elements), read before the
+    // products that need them
+    LDS const float* const tok_scales = (LDS const float*)(smem + L::kScales);
+    f32x4_t tok_ratio[kTau4];
+    if constexpr (FP8 && TOK && kSplitScales) {
+#pragma unroll
+      for (int tau = 0; tau < kTau4; ++tau)
+        tok_ratio[tau] = *(LDS const f32x4_t*)(tok_scales + kMaxSlotsPerSplit + h * kBlock +
+                                               16 * tau + 4 * lg);
+    }
 
     // S^T[token][row] for tokens 16*tau + ln16: 18 k-steps (2 RoPE, then 16
     // latent), 4 token tiles each.  Software pipeline: key fragments are
@@ -924,7 +1011,10 @@ void partial_kernel(const PartialParams p) {
 #pragma unroll
             for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
-              for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
+              for (int tau = 0; tau < kTau4; ++tau) {
+                if constexpr (TOK) scale_inplace4(sacc[rg][tau], tok_ratio[tau]);
+                else scale_inplace(sacc[rg][tau], pe_ratio);
+              }
           }
 #pragma unroll
           for (int j = 0; j < 2 * RG; ++j) {
@@ -1023,12 +1113,21 @@ void partial_kernel(const PartialParams p) {
     // token selections: the listed tokens in this virtual block (the rest of
     // the last one is fill, with no weight)
     const int n_here = TOK ? n_tok - h * kBlock : kBlock;
+    // fp8 token selections: the latent scales of the lane's tokens (each
+    // token's value is code * scale, its score scaled likewise)
+    f32x4_t tok_vm[kTau4];
+    if constexpr (FP8 && TOK) {
+#pragma unroll
+      for (int tau = 0; tau < kTau4; ++tau)
+        tok_vm[tau] = *(LDS const f32x4_t*)(tok_scales + h * kBlock + 16 * tau + 4 * lg);
+    }
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
       float bm = -INFINITY;
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) {
-        acc[rg][tau] *= s_mult;
+        if constexpr (FP8 && TOK) acc[rg][tau] *= tok_vm[tau] * s_mult;
+        else acc[rg][tau] *= s_mult;
         if (TOK && n_here < kBlock) {
 #pragma unroll
           for (int k = 0; k < 4; ++k)
@@ -1080,8 +1179,13 @@ void partial_kernel(const PartialParams p) {
         e1 = on[rg] ? e1 : 0.f;
       }
       psum[rg] += e0 + e1;
-      pb[rg][tau >> 1][(tau & 1) * 4 + k0] = (__bf16)(FP8 ? e0 * v_mult : e0);
-      pb[rg][tau >> 1][(tau & 1) * 4 + k0 + 1] = (__bf16)(FP8 ? e1 * v_mult : e1);
+      float vm0 = v_mult, vm1 = v_mult;
+      if constexpr (FP8 && TOK) {
+        vm0 = tok_vm[tau][k0];
+        vm1 = tok_vm[tau][k0 + 1];
+      }
+      pb[rg][tau >> 1][(tau & 1) * 4 + k0] = (__bf16)(FP8 ? e0 * vm0 : e0);
+      pb[rg][tau >> 1][(tau & 1) * 4 + k0 + 1] = (__bf16)(FP8 ? e1 * vm1 : e1);
     };
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
@@ -1191,10 +1295,14 @@ hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups,
                           hipStream_t s) {
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
-  if (sel_kind == kSelPerRow || sel_kind == kSelTokens) {
+  if (sel_kind == kSelPerRow) {
     if (kv != kKvBf16) return hipErrorInvalidValue;
-    if (sel_kind == kSelPerRow)
-      launch_kv<kKvBf16, kSelPerRow>(p, grid, row_groups, s);
+    launch_kv<kKvBf16, kSelPerRow>(p, grid, row_groups, s);
+  } else if (sel_kind == kSelTokens) {
+    if (kv == kKvFp8Shared)
+      launch_kv<kKvFp8Shared, kSelTokens>(p, grid, row_groups, s);
+    else if (kv == kKvFp8Split)
+      launch_kv<kKvFp8Split, kSelTokens>(p, grid, row_groups, s);
     else
       launch_kv<kKvBf16, kSelTokens>(p, grid, row_groups, s);
   } else if (kv == kKvFp8Shared)

@@ -418,7 +418,12 @@ CONFIGS = {
 def make(name, seed=None, **kw):
     """A named workload; `holder-{dense|sparse}-n{N}-h{H}[-jobs]` builds the
     holder experiment (see holder), `select-{tok|blk|dense}-b{B}-k{k}-c{c}[-h{H}]`
-    the selection-budget experiment (see selection)."""
+    the selection-budget experiment (see selection); a `-fp8` suffix on any of
+    these gives the same values as an e4m3 cache (one scale per block)."""
+    if name.endswith("-fp8") and name not in CONFIGS:
+        w = make(name[:-4], seed, **kw).to_fp8()
+        w.name = name
+        return w
     if name.startswith("select-"):
         parts = name.split("-")
         kw.update(kind=parts[1], n_req=int(parts[2][1:]), k=int(parts[3][1:]),

@@ -102,15 +102,57 @@ def test_tokens_top2048_of_32k_sampled():
     G.assert_parity(out[jobs], lse[jobs], ref_o, ref_l, "top-2048 of 32K")
 
 
-def test_tokens_reject_fp8_and_per_row():
+def _check8(w, n_splits=0, row_tile=0, what="", jobs=None):
+    out, lse = G.run_partial(G.upload(w), w.scale, n_splits=n_splits, row_tile=row_tile,
+                             tokens=True)
+    j = np.arange(w.sel.shape[0]) if jobs is None else np.asarray(jobs)
+    ref_o, ref_l = oracle.partial(w.q_lat[j], w.q_pe[j], w.ckv, w.kpe, w.table[j], w.sel[j],
+                                  w.scale, w.ckv_scale, w.kpe_scale, tokens=True)
+    return G.assert_parity(out[j], lse[j], ref_o, ref_l, what or w.name)
+
+
+def _fp8_tokens(seed, shared, **kw):
+    """A token case whose pool blocks have distinct fp8 scales (each block's
+    values drawn at its own magnitude), so every listed token carries its
+    own block's scale."""
+    w = W.random_case(seed, tokens=True, **kw)
+    P = w.ckv.shape[0]
+    mag = np.random.default_rng(seed).uniform(0.2, 3.0, P).astype(np.float32)
+    for name in ("ckv", "kpe"):
+        x = W.bf16_bits_to_f32(getattr(w, name)) * mag[:, None, None]
+        setattr(w, name, W.f32_to_bf16_bits(x))
+    return w.to_fp8(shared)
+
+
+@pytest.mark.parametrize("row_tile", [64, 128])
+@pytest.mark.parametrize("n_splits", [0, 1, 3])
+@pytest.mark.parametrize("shared", [True, False])
+def test_tokens_fp8(shared, n_splits, row_tile):
+    print(f"case: fp8 tokens shared={shared} splits={n_splits} row_tile={row_tile}", flush=True)
+    w = _fp8_tokens(760, shared, R=3, Mq=1, H=128, P=30, NB=12, K=300, sigma=0.6,
+                    allow_dup=True)
+    assert len(np.unique(w.ckv_scale)) > 20
+    _check8(w, n_splits, row_tile, f"fp8 tokens shared={shared} splits={n_splits}")
+
+
+@pytest.mark.parametrize("k", [1, 63, 65, 1025])
+@pytest.mark.parametrize("shared", [True, False])
+def test_tokens_fp8_ragged_and_padding(k, shared):
+    print(f"case: fp8 tokens k={k} shared={shared}", flush=True)
+    nb = max(2, -(-k // 64) + 3)
+    w = _fp8_tokens(770 + k, shared, R=2, Mq=2, H=16, P=nb + 5, NB=nb, K=k, sigma=0.8,
+                    allow_dup=True, pad_pattern="interleaved", n_valid=[k, max(0, k - 7)])
+    _check8(w, what=f"fp8 tokens k={k}")
+
+
+def test_tokens_fp8_top2048_of_32k_sampled():
+    print("case: fp8 tokens top-2048 of 32K", flush=True)
+    w = W.make("select-tok-b8-k2048-c32768").to_fp8(shared_scale=False)
+    _check8(w, jobs=[1, 6], what="fp8 top-2048 of 32K")
+
+
+def test_tokens_reject_per_row():
     w = W.random_case(750, R=1, Mq=2, H=16, P=8, NB=4, K=10, tokens=True)
-    w8 = w.to_fp8()
-    t = G.upload(w8)
-    with pytest.raises(mla.MlaError) as e:
-        mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"], t["sel"],
-                                w.scale, ckv_scale=t["ckv_scale"], kpe_scale=t["kpe_scale"],
-                                tokens=True)
-    assert e.value.status == mla.MLA_ERR_UNSUPPORTED
     t = G.upload(w)
     sel3 = torch.zeros((1, 2, 10), dtype=torch.int32, device=G.device())
     with pytest.raises(mla.MlaError) as e:
