@@ -168,8 +168,9 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
  * Every other argument, the result (T = the multiset of selected tokens)
  * and the layout rules are those of mla_sparse_partial_attn_ex; opts.n_splits
  * counts splits of the token slots (each split takes whole 64-token groups
- * of slots, at most 1024 slots).  bf16 caches only (MLA_ERR_UNSUPPORTED for
- * fp8); NB and P must not exceed 2^25 blocks (MLA_ERR_UNSUPPORTED).  An id
+ * of slots, at most 1024 slots).  bf16 or fp8 caches (a token takes the
+ * scales of its pool block); NB and P must not exceed 2^25 blocks
+ * (MLA_ERR_UNSUPPORTED).  An id
  * outside [0, 64 NB), or a table entry outside [0, P), is a caller error that
  * the call does not detect on the host: such a slot is skipped.
  */
