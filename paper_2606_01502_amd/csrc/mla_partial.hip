@@ -926,17 +926,14 @@ void partial_kernel(const PartialParams p) {
     // the loop.
     const int ln = lds_opaque(lane);
     const int ln16 = ln & 15, lg = ln >> 4;
-    // fp8 token selections: the RoPE / latent ratios of the lane's tokens
-    // 16 tau + 4 lg + k (its S^T accumulator elements), read before the
-    // products that need them
+    // fp8 token selections: the per-token scales of the lane's S^T elements
+    // (tokens 16 tau + 4 lg + k), read from LDS where they are used so that
+    // they hold no registers across the products
     LDS const float* const tok_scales = (LDS const float*)(smem + L::kScales);
-    f32x4_t tok_ratio[kTau4];
-    if constexpr (FP8 && TOK && kSplitScales) {
-#pragma unroll
-      for (int tau = 0; tau < kTau4; ++tau)
-        tok_ratio[tau] = *(LDS const f32x4_t*)(tok_scales + kMaxSlotsPerSplit + h * kBlock +
-                                               16 * tau + 4 * lg);
-    }
+    auto tok_scale4 = [&](int which, int tau) -> f32x4_t {
+      return *(LDS const f32x4_t*)(tok_scales + which * kMaxSlotsPerSplit + h * kBlock +
+                                   16 * tau + 4 * lg);
+    };
 
     // S^T[token][row] for tokens 16*tau + ln16: 18 k-steps (2 RoPE, then 16
     // latent), 4 token tiles each.  Software pipeline: key fragments are
@@ -1012,7 +1009,7 @@ void partial_kernel(const PartialParams p) {
             for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
               for (int tau = 0; tau < kTau4; ++tau) {
-                if constexpr (TOK) scale_inplace4(sacc[rg][tau], tok_ratio[tau]);
+                if constexpr (TOK) scale_inplace4(sacc[rg][tau], tok_scale4(1, tau));
                 else scale_inplace(sacc[rg][tau], pe_ratio);
               }
           }
@@ -1113,20 +1110,14 @@ void partial_kernel(const PartialParams p) {
     // token selections: the listed tokens in this virtual block (the rest of
     // the last one is fill, with no weight)
     const int n_here = TOK ? n_tok - h * kBlock : kBlock;
-    // fp8 token selections: the latent scales of the lane's tokens (each
-    // token's value is code * scale, its score scaled likewise)
-    f32x4_t tok_vm[kTau4];
-    if constexpr (FP8 && TOK) {
-#pragma unroll
-      for (int tau = 0; tau < kTau4; ++tau)
-        tok_vm[tau] = *(LDS const f32x4_t*)(tok_scales + h * kBlock + 16 * tau + 4 * lg);
-    }
+    // (fp8 token selections: each token's value is code * its block's
+    // latent scale, and its score is scaled likewise)
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) {
       float bm = -INFINITY;
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) {
-        if constexpr (FP8 && TOK) acc[rg][tau] *= tok_vm[tau] * s_mult;
+        if constexpr (FP8 && TOK) acc[rg][tau] *= tok_scale4(0, tau) * s_mult;
         else acc[rg][tau] *= s_mult;
         if (TOK && n_here < kBlock) {
 #pragma unroll
@@ -1181,8 +1172,8 @@ void partial_kernel(const PartialParams p) {
       psum[rg] += e0 + e1;
       float vm0 = v_mult, vm1 = v_mult;
       if constexpr (FP8 && TOK) {
-        vm0 = tok_vm[tau][k0];
-        vm1 = tok_vm[tau][k0 + 1];
+        vm0 = tok_scales[h * kBlock + 16 * tau + 4 * lg + k0];
+        vm1 = tok_scales[h * kBlock + 16 * tau + 4 * lg + k0 + 1];
       }
       pb[rg][tau >> 1][(tau & 1) * 4 + k0] = (__bf16)(FP8 ? e0 * vm0 : e0);
       pb[rg][tau >> 1][(tau & 1) * 4 + k0 + 1] = (__bf16)(FP8 ? e1 * vm1 : e1);
