@@ -100,8 +100,7 @@ typedef struct {
  *                                     rows) on the job's chunk, each with its
  *                                     own selection (Section 6.3).  Blocks that
  *                                     several rows select are read once for
- *                                     all of them.  bf16 caches only
- *                                     (MLA_ERR_UNSUPPORTED for fp8); NB times
+ *                                     all of them.  NB times
  *                                     the query rows one row tile spans (128
  *                                     rows, or 64 when 128 would span more
  *                                     than 64 query rows) must not exceed

@@ -202,8 +202,6 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     if (chunk_block_table->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_block_table: shape must be [R, NB]");
     if (sel_block_ids->shape[0] != R || (per_row && sel_block_ids->shape[1] != Mq))
       return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K] or [R, Mq, K]");
-    if (per_row && fp8)
-      return fail(MLA_ERR_UNSUPPORTED, "per-row selections need a bf16 cache");
     if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
     if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
     if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||
@@ -282,7 +280,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     // per-row selections whose tile slots all fit one list split by logical
     // block: every split then scans all slots and the rows that chose a block
     // in different slots still share its load
-    const bool by_id = per_row && tile_qrows > 1 && K * tile_qrows <= mla::kMaxSlotsPerSplit;
+    // entries one split's list holds (per-row selections with an fp8 cache:
+    // half a list, see the kernel's LDS layout)
+    const int64_t list_cap = per_row && fp8 ? mla::kPerRowListFp8 : mla::kMaxSlotsPerSplit;
+    const bool by_id = per_row && tile_qrows > 1 && K * tile_qrows <= list_cap;
     int64_t S;
     if (opts && opts->n_splits > 0) {
       S = std::min<int64_t>(opts->n_splits, std::max<int64_t>(by_id ? NB : K, 1));
@@ -308,9 +309,9 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       sps = std::min<int64_t>(sps, mla::kMaxSlotsPerSplit);
       S = std::max<int64_t>(1, (K + sps - 1) / sps);
     } else if (!by_id) {
-      S = std::max<int64_t>(S, (K * tile_qrows + mla::kMaxSlotsPerSplit - 1) / mla::kMaxSlotsPerSplit);
+      S = std::max<int64_t>(S, (K * tile_qrows + list_cap - 1) / list_cap);
       sps = std::max<int64_t>(1, (K + S - 1) / S);
-      if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, mla::kMaxSlotsPerSplit / tile_qrows));
+      if (per_row) sps = std::min<int64_t>(sps, std::max<int64_t>(1, list_cap / tile_qrows));
       S = std::max<int64_t>(1, (K + sps - 1) / sps);
     }
     if (R * row_tiles * S > INT32_MAX) return fail(MLA_ERR_UNSUPPORTED, "grid too large");

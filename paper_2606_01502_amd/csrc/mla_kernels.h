@@ -101,6 +101,7 @@ constexpr int kKvFp8Split = 2;   // e4m3, separate ckv and kpe scales per block
 // its stage area, NB * (query rows of the tile) 16-bit counters.
 constexpr int kPerRowCounterBytes = 2 * 64 * 1152;  // the bf16 stage area
 constexpr int kPerRowMaxRows = 64;                  // query rows per row tile (mask bits)
+constexpr int kPerRowListFp8 = kMaxSlotsPerSplit / 2;  // list entries per split, fp8 caches
 
 // Selection kinds: one block selection per job, one per query row, or one
 // token selection per job (bf16 caches only for the last two).

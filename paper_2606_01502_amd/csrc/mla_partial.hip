@@ -82,10 +82,17 @@ struct Layout {
   static constexpr int kList = kNum * kStage;
   static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
   static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
-  static constexpr int kMasks = kWaveCnt + 16;  // per-row selections: 64-bit row mask per entry
-  static constexpr int kTotal = kMasks;
-  static constexpr int kTotalPerRow = kMasks + kMaxSlotsPerSplit * 8;
+  static constexpr int kTotal = kWaveCnt + 16;
+  // Per-row selections: a 64-bit row mask per list entry.  bf16: after the
+  // rest, for a full list.  fp8 (whose four stages leave no room for that):
+  // half a list, its scales and masks sharing the scale area.
+  static constexpr int kPerRowCap = FP8 ? kMaxSlotsPerSplit / 2 : kMaxSlotsPerSplit;
+  static constexpr int kMasks = FP8 ? kScales + kPerRowCap * 8 : kTotal;
+  static constexpr int kTotalPerRow = FP8 ? kTotal : kMasks + kPerRowCap * 8;
 };
+static_assert(Layout<true>::kMasks + Layout<true>::kPerRowCap * 8 <= Layout<true>::kWaveCnt,
+              "fp8 per-row scales and masks fit the scale area");
+static_assert(Layout<true>::kPerRowCap == kPerRowListFp8, "per-row fp8 list size");
 static_assert(Layout<true>::kTotal <= 160 * 1024 && Layout<false>::kTotalPerRow <= 160 * 1024,
               "LDS budget");
 static_assert(kPerRowCounterBytes <= Layout<false>::kNum * Layout<false>::kStage,
@@ -601,6 +608,8 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
 // come in ascending logical-block order.  The counters (16 bits per (block,
 // row) of the blocks taken; at most nslots each) use the stage area, which is
 // free until the first load is issued.  Returns the number of entries.
+// fp8: each entry also gets its block's latent scale and RoPE / latent ratio.
+template <bool FP8>
 __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, int slot0,
                                                int nslots, int id0, int id_step, int i0, int n_i,
                                                LDS uint8_t* smem, LDS int* list,
@@ -609,7 +618,8 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   LDS uint32_t* cnt = (LDS uint32_t*)smem;
   LDS const uint16_t* cnt16 = (LDS const uint16_t*)smem;
-  LDS int* wave_cnt = (LDS int*)(smem + Layout<false>::kWaveCnt);
+  LDS int* wave_cnt = (LDS int*)(smem + Layout<FP8>::kWaveCnt);
+  LDS float* scales = (LDS float*)(smem + Layout<FP8>::kScales);
   const int n_ids = id0 < p.NB ? (p.NB - id0 + id_step - 1) / id_step : 0;
   const int n_words = (n_ids * n_i + 1) >> 1;
   for (int w = tid; w < n_words; w += 256) cnt[w] = 0u;
@@ -652,12 +662,21 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
     }
     if (kmax > 0) {
       const int bb = p.table[r * p.table_s0 + id];
+      float sc = 1.f, ratio = 1.f;
+      if constexpr (FP8) {
+        sc = p.ckv_scale[bb];
+        ratio = p.kpe_scale[bb] / sc;
+      }
       for (int k = 0; k < kmax; ++k) {
         uint64_t m = 0;
         for (int ii = 0; ii < n_i; ++ii)
           if ((int)cnt16[u * n_i + ii] > k) m |= 1ull << ii;
         list[off + k] = bb;
         masks[off + k] = m;
+        if constexpr (FP8) {
+          scales[2 * (off + k)] = sc;
+          scales[2 * (off + k) + 1] = ratio;
+        }
       }
     }
     n_valid += total;
@@ -742,7 +761,6 @@ void partial_kernel(const PartialParams p) {
   constexpr bool FP8 = KV != kKvBf16;
   constexpr bool PR = SEL == kSelPerRow;   // a block selection per query row
   constexpr bool TOK = SEL == kSelTokens;  // token selections, 64 to a virtual block
-  static_assert(!(PR && FP8), "per-row selections: bf16 caches only");
   constexpr bool kSplitScales = KV == kKvFp8Split;
   using L = Layout<FP8>;
   constexpr int kTau4 = kBlock / 16;   // 16-token tiles per block
@@ -780,8 +798,8 @@ void partial_kernel(const PartialParams p) {
     // slot), so that rows which chose one block in different slots share its
     // load; or by slot range when a tile's slots may not fit one list
     n_valid = p.split_by_id
-                  ? compact_per_row(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
-                  : compact_per_row(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
+                  ? compact_per_row<FP8>(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
+                  : compact_per_row<FP8>(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
   } else if constexpr (TOK) {
     n_tok = compact_tokens<FP8>(p, r, slot0, nslots, smem, tid);
     n_valid = (n_tok + kBlock - 1) / kBlock;
@@ -1287,8 +1305,12 @@ hipError_t launch_partial(const PartialParams& p, int R, int kv, int row_groups,
   const int grid = R * p.row_tiles * p.n_splits;
   if (grid <= 0) return hipSuccess;
   if (sel_kind == kSelPerRow) {
-    if (kv != kKvBf16) return hipErrorInvalidValue;
-    launch_kv<kKvBf16, kSelPerRow>(p, grid, row_groups, s);
+    if (kv == kKvFp8Shared)
+      launch_kv<kKvFp8Shared, kSelPerRow>(p, grid, row_groups, s);
+    else if (kv == kKvFp8Split)
+      launch_kv<kKvFp8Split, kSelPerRow>(p, grid, row_groups, s);
+    else
+      launch_kv<kKvBf16, kSelPerRow>(p, grid, row_groups, s);
   } else if (sel_kind == kSelTokens) {
     if (kv == kKvFp8Shared)
       launch_kv<kKvFp8Shared, kSelTokens>(p, grid, row_groups, s);

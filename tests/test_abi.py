@@ -98,8 +98,6 @@ def test_per_row_selection_host_checks():
     assert st == mla.MLA_ERR_INVALID_ARGUMENT and "[R, Mq, K]" in msg
     st, msg = _cpu_call((3, 3))  # R mismatch
     assert st == mla.MLA_ERR_INVALID_ARGUMENT
-    st, msg = _cpu_call((2, 3, 3), fp8=True)
-    assert st == mla.MLA_ERR_UNSUPPORTED and "bf16" in msg
     st, msg = _cpu_call((2, 3, 3), NB=40000)  # per-row counters would not fit in LDS
     assert st == mla.MLA_ERR_UNSUPPORTED and "NB" in msg
     st, msg = _cpu_call((2, 3, 3, 1))  # 4-d selection

@@ -112,13 +112,28 @@ def test_per_row_many_requesters_sampled():
     G.assert_parity(out[:, rows], lse[:, rows], ref_o, ref_l, "per-row 64 requesters")
 
 
-def test_per_row_rejects_fp8_cache():
-    w = W.random_case(690, R=1, Mq=2, H=16, P=8, NB=4, K=3, per_row=True).to_fp8()
+def _check8(w, n_splits=0, row_tile=0, what=""):
     t = G.upload(w)
-    with pytest.raises(mla.MlaError) as e:
-        mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"], t["sel"],
-                                w.scale, ckv_scale=t["ckv_scale"], kpe_scale=t["kpe_scale"])
-    assert e.value.status == mla.MLA_ERR_UNSUPPORTED
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits, row_tile=row_tile)
+    ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                                  w.ckv_scale, w.kpe_scale)
+    return G.assert_parity(out, lse, ref_o, ref_l, what)
+
+
+@pytest.mark.parametrize("row_tile", [64, 128])
+@pytest.mark.parametrize("shared", [True, False])
+@pytest.mark.parametrize("mq,h,k", [(8, 16, 6), (4, 32, 140), (3, 40, 9)])
+def test_per_row_fp8(mq, h, k, shared, row_tile):
+    """fp8 caches with a selection per query row: block splits (short
+    selections) and slot-range splits (140 slots x 4 query rows of a
+    128-row tile overflow the fp8 per-row list of 512), duplicates and
+    padding, both scale layouts."""
+    print(f"case: per-row fp8 {mq}x{h} K={k} shared={shared} row_tile={row_tile}", flush=True)
+    w = W.random_case(690 + mq + h + k, R=2, Mq=mq, H=h, P=60, NB=50, K=k, sigma=0.7,
+                      allow_dup=True, pad_pattern="interleaved", per_row=True, shared_frac=0.6)
+    w8 = w.to_fp8(shared)
+    for s_ in (0, 3):
+        _check8(w8, s_, row_tile, f"per-row fp8 {mq}x{h} K={k} splits={s_}")
 
 
 @pytest.mark.parametrize("kind", ["dense", "sparse"])
