@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define MLA_SPARSE_VERSION 1
+#define MLA_SPARSE_VERSION 2
 
 #define MLA_DLAT 512  /* latent width = d_v (Section 3.2)                    */
 #define MLA_DPE 64    /* decoupled-RoPE width = d_qk - d_v (Section 3.2)      */

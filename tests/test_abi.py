@@ -29,7 +29,9 @@ def test_library_exports_every_declared_symbol():
 def test_version_and_error_string_without_gpu():
     from paper_2606_01502_amd import mla
     lib = mla.load()
-    assert lib.mla_version() == 1
+    with open(os.path.join(ROOT, "include", "mla_sparse.h")) as f:
+        want = int(re.search(r"#define MLA_SPARSE_VERSION (\d+)", f.read()).group(1))
+    assert lib.mla_version() == want == 2
     assert lib.mla_last_error() == b""
 
 
