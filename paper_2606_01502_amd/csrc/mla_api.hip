@@ -347,12 +347,19 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     p.lse = (float*)out_lse->data;
     p.lse_s0 = out_lse->stride[0]; p.lse_s1 = out_lse->stride[1]; p.lse_s2 = out_lse->stride[2];
     if (S > 1) {
+      // split rows, then their scales (fp16 rows only), then their lse values.
+      // fp16 rows halve the workspace round trip, which pays once it moves
+      // tens of MB; small workspaces keep fp32 rows, whose epilogue and
+      // combine are a little shorter (the latency-bound case)
       const size_t n_part_rows = (size_t)R * S * rows;
-      const size_t o_bytes = n_part_rows * MLA_DLAT * sizeof(float);
+      p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
+      const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
       void* ws = nullptr;
-      if ((st = get_workspace(hs, o_bytes + n_part_rows * sizeof(float), &ws)) != MLA_OK) return st;
-      p.ws_o = (float*)ws;
-      p.ws_lse = (float*)((char*)ws + o_bytes);
+      if ((st = get_workspace(hs, o_bytes + 2 * n_part_rows * sizeof(float), &ws)) != MLA_OK) return st;
+      p.ws_o32 = (float*)ws;
+      p.ws_o16 = (uint16_t*)ws;
+      p.ws_scale = (float*)((char*)ws + o_bytes);
+      p.ws_lse = p.ws_scale + n_part_rows;
     }
     const int kv = !fp8 ? mla::kKvBf16
                  : (ckv_pool->block_scale == kpe_pool->block_scale ? mla::kKvFp8Shared
@@ -362,7 +369,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     if (e != hipSuccess) return fail(MLA_ERR_HIP, std::string("partial kernel launch: ") + hipGetErrorString(e));
     if (S > 1) {
       mla::CombineParams c{};
-      c.ws_o = p.ws_o;
+      c.ws_f16 = p.ws_f16;
+      c.ws_o32 = p.ws_o32;
+      c.ws_o16 = p.ws_o16;
+      c.ws_scale = p.ws_scale;
       c.ws_lse = p.ws_lse;
       c.R = (int32_t)R; c.S = (int32_t)S; c.Mq = (int32_t)Mq; c.H = (int32_t)H; c.rows = (int32_t)rows;
       c.out = p.out; c.out_s0 = p.out_s0; c.out_s1 = p.out_s1; c.out_s2 = p.out_s2;

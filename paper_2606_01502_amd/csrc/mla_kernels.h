@@ -13,6 +13,8 @@ constexpr int kBlock = 64;   // tokens per cache block
 constexpr int kThreads = 256;             // merge / combine workgroup size
 constexpr int kMaxSlotsPerSplit = 1024;   // selected-slot range one workgroup handles
 constexpr int kMaxParts = 64;
+// split-K workspaces of at least this many fp32 row bytes store fp16 rows
+constexpr int64_t kWsHalfMinBytes = 48ll << 20;
 
 // Partial attention over one (job, row tile, slot range) per workgroup.
 struct PartialParams {
@@ -42,13 +44,22 @@ struct PartialParams {
   int64_t out_s0, out_s1, out_s2;
   float* lse;
   int64_t lse_s0, lse_s1, lse_s2;
-  float* ws_o;    // [R][S][rows][512]
-  float* ws_lse;  // [R][S][rows]
+  // split-K workspace, [R][S][rows] split rows with their lse: fp32 rows, or
+  // when ws_f16 is set (large workspaces) fp16 rows divided by the row's
+  // largest magnitude, which ws_scale holds
+  int32_t ws_f16;
+  float* ws_o32;     // [R][S][rows][512]
+  uint16_t* ws_o16;  // [R][S][rows][512] fp16 bits
+  float* ws_scale;   // [R][S][rows]
+  float* ws_lse;     // [R][S][rows]
 };
 
 // Combine of the S split partials of every job into the caller's outputs.
 struct CombineParams {
-  const float* ws_o;
+  int32_t ws_f16;  // see PartialParams
+  const float* ws_o32;
+  const uint16_t* ws_o16;
+  const float* ws_scale;
   const float* ws_lse;
   int32_t R, S, Mq, H, rows;
   float* out;

@@ -38,11 +38,39 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Part rows as fp32 (callers' partials) or as fp16 divided by a per-row
+// scale (the split-K workspace): columns 4 lane .. +3 and 256 + 4 lane .. +3.
+struct F32Rows {
+  template <typename RowAt>
+  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
+                                              f32x4_t& v1) {
+    const float* r = row_at(j);
+    v0 = *(const f32x4_t*)(r + 4 * lane);
+    v1 = *(const f32x4_t*)(r + 256 + 4 * lane);
+  }
+};
+
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+struct F16Rows {
+  template <typename RowAt>
+  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
+                                              f32x4_t& v1) {
+    const uint16_t* r = row_at(j);
+    const f16x4_t a = *(const f16x4_t*)(r + 4 * lane);
+    const f16x4_t b = *(const f16x4_t*)(r + 256 + 4 * lane);
+    v0 = f32x4_t{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
+    v1 = f32x4_t{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
+  }
+};
+
 // Merge n parts of one row.  lse_at(j): part j's lse; row_at(j): part j's
-// 512 floats.  Writes the 512 outputs at out and returns the merged lse.
-template <typename LseAt, typename RowAt>
-__device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, float* out,
-                                           int lane) {
+// row (Rows says how to read it); scale_at(j): the factor part j's stored
+// values carry (1 for fp32 parts).  Writes the 512 outputs at out and
+// returns the merged lse.
+template <typename Rows, typename LseAt, typename RowAt, typename ScaleAt>
+__device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, ScaleAt scale_at,
+                                           float* out, int lane) {
   float m = -INFINITY;
   for (int j0 = 0; j0 < n; j0 += 64) {
     const int j = j0 + lane;
@@ -62,7 +90,7 @@ __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, fl
     for (int j0 = 0; j0 < n; j0 += 64) {
       const int j = j0 + lane;
       const float l = j < n ? lse_at(j) : -INFINITY;
-      const float w = l != -INFINITY ? __expf(l - lse) : 0.f;
+      const float w = l != -INFINITY ? __expf(l - lse) * scale_at(j) : 0.f;
       uint64_t live = __ballot(l != -INFINITY);
       while (live) {
         int idx[kBatch];
@@ -77,13 +105,8 @@ __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, fl
         }
         f32x4_t v0[kBatch], v1[kBatch];
 #pragma unroll
-        for (int k = 0; k < kBatch; ++k) {
-          if (k < cnt) {
-            const float* r = row_at(j0 + idx[k]);
-            v0[k] = *(const f32x4_t*)(r + 4 * lane);
-            v1[k] = *(const f32x4_t*)(r + 256 + 4 * lane);
-          }
-        }
+        for (int k = 0; k < kBatch; ++k)
+          if (k < cnt) Rows::load(row_at, j0 + idx[k], lane, v0[k], v1[k]);
 #pragma unroll
         for (int k = 0; k < kBatch; ++k) {
           if (k < cnt) {
@@ -110,9 +133,9 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
   const int i = rem / p.H, h = rem - (rem / p.H) * p.H;
   const int64_t lo = b * p.l_s0 + i * p.l_s1 + h * p.l_s2;
   const int64_t oo = b * p.o_s0 + i * p.o_s1 + h * p.o_s2;
-  const float lse = merge_row(
+  const float lse = merge_row<F32Rows>(
       p.n_parts, [&](int j) { return p.lse[j][lo]; }, [&](int j) { return p.o[j] + oo; },
-      p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
+      [](int) { return 1.f; }, p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
   if (p.out_lse && lane == 0) p.out_lse[b * p.ol_s0 + i * p.ol_s1 + h * p.ol_s2] = lse;
 }
 
@@ -125,10 +148,15 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineParams p
   const int row = grow - r * p.rows;
   const int64_t base = (int64_t)r * p.S * p.rows + row;  // split j of (r, row) at base + j*rows
   const int i = row / p.H, h = row - (row / p.H) * p.H;
-  const float lse = merge_row(
-      p.S, [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; },
-      [&](int j) { return p.ws_o + (base + (int64_t)j * p.rows) * kDLat; },
-      p.out + r * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
+  float* out = p.out + r * p.out_s0 + i * p.out_s1 + h * p.out_s2;
+  auto lse_at = [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; };
+  const float lse =
+      p.ws_f16 ? merge_row<F16Rows>(
+                     p.S, lse_at, [&](int j) { return p.ws_o16 + (base + (int64_t)j * p.rows) * kDLat; },
+                     [&](int j) { return p.ws_scale[base + (int64_t)j * p.rows]; }, out, lane)
+               : merge_row<F32Rows>(
+                     p.S, lse_at, [&](int j) { return p.ws_o32 + (base + (int64_t)j * p.rows) * kDLat; },
+                     [](int) { return 1.f; }, out, lane);
   if (lane == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2] = lse;
 }
 

@@ -115,6 +115,20 @@ def test_many_slots_split_limits():
         _check_case(w, s, f"many slots splits={s}")
 
 
+@pytest.mark.parametrize("n_splits", [2, 32])
+def test_split_workspace_formats(n_splits):
+    """Two splits keep an fp32 workspace (8 MB); thirty-two reach the size
+    (134 MB) at which split rows are stored as scaled fp16.  Both against
+    the oracle on three of the sixteen jobs."""
+    print(f"case: workspace format splits={n_splits}", flush=True)
+    w = W.random_case(111, R=16, Mq=1, H=128, P=80, NB=70, K=64, sigma=0.5)
+    t = G.upload(w)
+    out, lse = G.run_partial(t, w.scale, n_splits=n_splits)
+    jobs = [0, 7, 15]
+    ref_o, ref_l = _oracle(w, jobs)
+    G.assert_parity(out[jobs], lse[jobs], ref_o, ref_l, f"workspace splits={n_splits}")
+
+
 def test_split_invariance_gpu_only():
     """Different split plans agree with each other within rounding."""
     print("case: split invariance", flush=True)
