@@ -37,6 +37,15 @@
 // (the kKvFp8Split instance) the RoPE part of the scores is first weighted by
 // the RoPE / latent scale ratio, before the latent part is added.
 //
+// Selections (the SEL template parameter): one list of 64-token blocks per
+// job (shared by its rows); one list per query row (a holder serving several
+// routed requesters, Section 6.3), where a row tile loads the union of its
+// rows' blocks once and masks every row to its own multiset; or single
+// tokens (an indexer's top-k, Section 6.3's selection budgets), gathered 64
+// at a time into the same stage layout, each with its own block's fp8
+// scales.  Splits of a large workspace store their rows as fp16 scaled by the
+// row's largest magnitude.
+//
 // LDS swizzles (token t of the block, 16-byte chunk c of its row) are
 // described with bf16_key and fp8_key below.
 
