@@ -54,19 +54,29 @@ def parse():
     return ap.parse_args()
 
 
+def code_fingerprint(path):
+    """SHA-256 of a C/HIP source with its comments and white space removed:
+    it changes with the code, not with edits of comments."""
+    import hashlib
+    import re
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()
+
+
 def counted_traffic(workload, n_splits, kernel="partial_kernel"):
     """HBM bytes per launch of the kernel from the committed rocprofv3
     counter summary (FETCH_SIZE / WRITE_SIZE scaled by a known-size copy), or
     None when that summary is for another workload or an older kernel source."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.json")
     if n_splits != 0 or not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    with open(os.path.join(ROOT, d["source"]), "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
-    return d["traffic_bytes"] if sha == d["source_sha256"] else None
+    fp = code_fingerprint(os.path.join(ROOT, d["source"]))
+    return d["traffic_bytes"] if fp == d.get("source_code_fingerprint") else None
 
 
 def algorithmic(w):
