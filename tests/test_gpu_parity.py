@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import oracle
-from paper_2606_01502_amd import workloads as W
+from paper_2606_01502_amd import mla, workloads as W
 from tests import gpu_helpers as G
 
 pytestmark = pytest.mark.gpu
@@ -158,3 +158,45 @@ def test_dsv3_one_request_config():
 def test_few_head_config_full():
     print("case: few-head full", flush=True)
     _check_case(W.few_head())
+
+
+@pytest.mark.parametrize("n_splits", [1, 3])
+@pytest.mark.parametrize("tokens", [False, True])
+def test_strided_queries_and_outputs(n_splits, tokens):
+    """q_lat / q_pe as views with padded strides on the R, Mq and H dims, and
+    out_lat / out_lse written into views of larger buffers: the results equal
+    those of contiguous tensors bit for bit, and nothing outside the views
+    is written."""
+    print(f"case: strided splits={n_splits} tokens={tokens}", flush=True)
+    w = W.random_case(112, R=3, Mq=2, H=40, P=20, NB=9, K=100 if tokens else 6, sigma=0.7,
+                      tokens=tokens)
+    t = G.upload(w)
+    dev = G.device()
+    R, Mq, H = 3, 2, 40
+    # queries inside larger buffers: padding on every outer dim
+    big_l = torch.zeros((R + 1, Mq + 1, H + 3, 512 + 64), dtype=torch.bfloat16, device=dev)
+    big_p = torch.zeros((R, Mq, H + 5, 64 + 32), dtype=torch.bfloat16, device=dev)
+    ql = big_l[1:, :Mq, 2:2 + H, 64:576]
+    qp = big_p[:, :, 3:3 + H, 16:80]
+    ql.copy_(t["q_lat"])
+    qp.copy_(t["q_pe"])
+    out_big = torch.full((R, Mq, H + 2, 512 + 8), 7.0, dtype=torch.float32, device=dev)
+    lse_big = torch.full((R, Mq + 1, H + 4), 7.0, dtype=torch.float32, device=dev)
+    out_v = out_big[:, :, 1:1 + H, 4:516]
+    lse_v = lse_big[:, 1:, 2:2 + H]
+    mla.sparse_partial_attn(ql, qp, t["ckv"], t["kpe"], t["table"], t["sel"], w.scale, out_v,
+                            lse_v, n_splits=n_splits, tokens=tokens)
+    ref_o, ref_l = mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"],
+                                           t["sel"], w.scale, n_splits=n_splits, tokens=tokens)
+    torch.cuda.synchronize()
+    assert torch.equal(out_v, ref_o) and torch.equal(lse_v, ref_l)
+    mask = torch.ones_like(out_big, dtype=torch.bool)
+    mask[:, :, 1:1 + H, 4:516] = False
+    assert bool((out_big[mask] == 7.0).all()), "a write landed outside out_lat's view"
+    mask = torch.ones_like(lse_big, dtype=torch.bool)
+    mask[:, 1:, 2:2 + H] = False
+    assert bool((lse_big[mask] == 7.0).all()), "a write landed outside out_lse's view"
+    o_or, l_or = _oracle(w) if not tokens else oracle.partial(
+        w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, tokens=True)
+    G.assert_parity(out_v.cpu().numpy().astype(np.float64), lse_v.cpu().numpy().astype(np.float64),
+                    o_or, l_or, "strided")
