@@ -1256,13 +1256,15 @@ void partial_kernel(const PartialParams p) {
   }
 
   // ---- epilogue: normalise and write each row (out = O / l, lse = m + ln l).
-  // The accumulator layout gives a lane 16 bytes of a row per column tile, so
-  // each row group is first transposed through LDS (a 32 KiB area per wave,
-  // 16-byte chunk c of row rr in slot c ^ rr) and then stored one contiguous
-  // 1 KiB half row per instruction.  Splits of a large workspace write their
-  // rows as fp16 values divided by the row's largest magnitude (kept in fp32
-  // beside the lse): half the bytes of fp32, at 2^-11 of that magnitude,
-  // which the combine multiplies back.
+  // The accumulator layout gives lane (n16, g) 16-byte chunk 4 dt + g of row
+  // n16 for every column tile dt: fp32 rows are stored straight from there
+  // (64-byte runs per row and instruction, which the L2 joins into whole
+  // lines; measured faster than transposing through LDS first).  Splits of a
+  // large workspace write their rows as fp16 values divided by the row's
+  // largest magnitude (kept in fp32 beside the lse): half the bytes of fp32,
+  // at 2^-11 of that magnitude, which the combine multiplies back; those
+  // rows are transposed through LDS (a 32 KiB area per wave, 16-byte chunk c
+  // of row rr in slot c ^ rr) and stored as contiguous 1 KiB rows.
   const bool direct = p.n_splits == 1;
   const bool half = !direct && p.ws_f16;
   const int64_t part = (int64_t)r * p.n_splits + s_idx;
@@ -1276,66 +1278,68 @@ void partial_kernel(const PartialParams p) {
     const int row = row0 + n16;
     const float lse = l_tot > 0.f ? (m_run[rg] + __log2f(l_tot)) * kLn2 : -INFINITY;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    float amax = 0.f;  // the row's largest |out| (split rows only)
+    if (!half) {
+      if (g == 0 && row < p.rows) {
+        if (direct) {
+          const int i = row / p.H, hd = row - (row / p.H) * p.H;
+          p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
+        } else {
+          p.ws_lse[part * p.rows + row] = lse;
+        }
+      }
+      if (row < p.rows) {
+        float* dst;
+        if (direct) {
+          const int i = row / p.H, hd = row - (row / p.H) * p.H;
+          dst = p.out + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
+        } else {
+          dst = p.ws_o32 + (part * p.rows + row) * kDLat;
+        }
+#pragma unroll
+        for (int dt = 0; dt < 32; ++dt) {
+          f32x4_t v = O[dt][rg];
+          asm volatile("" : "+a"(v));  // read in place, no copy back
+          *(f32x4_t*)(dst + 4 * (4 * dt + g)) = v * inv;
+        }
+      }
+      continue;
+    }
+    // scaled fp16 rows: the row's largest magnitude, then the rows through LDS
+    float amax = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 32; ++dt) {
-      const f32x4_t v = scale_acc(O[dt][rg], inv);
-      if (half)
-        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+      f32x4_t v = O[dt][rg];
+      asm volatile("" : "+a"(v));
+      v *= inv;
+      amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
       *(LDS f32x4_t*)(stage + n16 * 2048 + (((4 * dt + g) ^ n16) << 4)) = v;
     }
     amax = xor_max(amax);
     const float row_scale = amax > 0.f ? amax : 1.f;
     if (g == 0 && row < p.rows) {
-      if (direct) {
-        const int i = row / p.H, hd = row - (row / p.H) * p.H;
-        p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
-      } else {
-        p.ws_lse[part * p.rows + row] = lse;
-        if (half) p.ws_scale[part * p.rows + row] = row_scale;
-      }
+      p.ws_lse[part * p.rows + row] = lse;
+      p.ws_scale[part * p.rows + row] = row_scale;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
-    if (half) {
-      // lane ln stores 16-byte chunk ln of row rr's 1 KiB fp16 row: columns
-      // 8 ln .. 8 ln + 7, i.e. fp32 chunks 2 ln and 2 ln + 1 of the stage
-      const float inv_scale_own = 1.f / row_scale;
+    // lane ln stores 16-byte chunk ln of row rr's 1 KiB fp16 row: columns
+    // 8 ln .. 8 ln + 7, i.e. fp32 chunks 2 ln and 2 ln + 1 of the stage
+    const float inv_scale_own = 1.f / row_scale;
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int rw = row0 + rr;
-        if (rw >= p.rows) break;
-        // lane rr holds row rr's scale; a constant lane index reads it into
-        // a scalar register
-        const float is = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, inv_scale_own), rr));
-        const f32x4_t a = *(const LDS f32x4_t*)(stage + rr * 2048 + (((2 * ln) ^ rr) << 4));
-        const f32x4_t b = *(const LDS f32x4_t*)(stage + rr * 2048 + (((2 * ln + 1) ^ rr) << 4));
-        u32x4_t h;
-        h[0] = pack_f16(a[0] * is, a[1] * is);
-        h[1] = pack_f16(a[2] * is, a[3] * is);
-        h[2] = pack_f16(b[0] * is, b[1] * is);
-        h[3] = pack_f16(b[2] * is, b[3] * is);
-        *(u32x4_t*)(p.ws_o16 + (part * p.rows + rw) * kDLat + 8 * ln) = h;
-      }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // reads of this row group done before it is overwritten
-      continue;
-    }
-#pragma unroll 4
     for (int rr = 0; rr < 16; ++rr) {
       const int rw = row0 + rr;
       if (rw >= p.rows) break;
-      float* dst;
-      if (direct) {
-        const int i = rw / p.H, hd = rw - (rw / p.H) * p.H;
-        dst = p.out + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
-      } else {
-        dst = p.ws_o32 + (part * p.rows + rw) * kDLat;
-      }
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int c = 64 * half + ln;
-        *(f32x4_t*)(dst + 4 * c) = *(const LDS f32x4_t*)(stage + rr * 2048 + ((c ^ rr) << 4));
-      }
+      // lane rr holds row rr's scale; a constant lane index reads it into a
+      // scalar register
+      const float is = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, inv_scale_own), rr));
+      const f32x4_t a = *(const LDS f32x4_t*)(stage + rr * 2048 + (((2 * ln) ^ rr) << 4));
+      const f32x4_t b = *(const LDS f32x4_t*)(stage + rr * 2048 + (((2 * ln + 1) ^ rr) << 4));
+      u32x4_t h;
+      h[0] = pack_f16(a[0] * is, a[1] * is);
+      h[1] = pack_f16(a[2] * is, a[3] * is);
+      h[2] = pack_f16(b[0] * is, b[1] * is);
+      h[3] = pack_f16(b[2] * is, b[3] * is);
+      *(u32x4_t*)(p.ws_o16 + (part * p.rows + rw) * kDLat + 8 * ln) = h;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // reads of this row group done before it is overwritten
   }
