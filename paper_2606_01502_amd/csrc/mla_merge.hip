@@ -26,16 +26,39 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kRowsPerBlock = kThreads / 64;  // one wave per row
 constexpr int kBatch = 8;                    // parts in flight per wave
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+// Reductions over the 64 lanes of a wave, all in VGPRs: the gfx950 row-swap
+// permutes pair lane l with l ^ 32 and then with l ^ 16 (with both operands
+// holding v, the two results at a lane are v[l] and its partner's value);
+// row rotations by 8, 4, 2 and 1 lanes (DPP) then cover the 16 lanes of a
+// row.  Every lane ends with the same value: each step combines the same two
+// values at both lanes of a pair, in either order.
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  uint32_t u = __float_as_uint(v);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  v = op(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  u = __float_as_uint(v);
+  const auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = op(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  // DPP row_ror:n = 0x120 + n
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xf, 0xf, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xf, 0xf, false)));
   return v;
 }
 
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  return wave_reduce(v, [](float x, float y) { return x + y; });
+}
+
+// A lane's value read by every lane (src wave-uniform).
+__device__ __forceinline__ float lane_value(float v, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
 }
 
 // Part rows as fp32 (callers' partials) or as fp16 divided by a per-row
@@ -110,7 +133,7 @@ __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, Sc
 #pragma unroll
         for (int k = 0; k < kBatch; ++k) {
           if (k < cnt) {
-            const float wk = __shfl(w, idx[k]);
+            const float wk = lane_value(w, idx[k]);
             acc0 += wk * v0[k];
             acc1 += wk * v1[k];
           }
