@@ -120,6 +120,13 @@ typedef struct {
  * does not change the result beyond rounding.  A selected id outside
  * [0, NB), or a table entry outside [0, P), is a caller error that this call
  * does not detect on the host: such a slot is skipped (treated as empty).
+ *
+ * Split-K workspace: when a job is split, the library keeps one grow-only
+ * device buffer per (device, stream), allocated on first need (a larger
+ * need synchronizes the stream and reallocates; MLA_ERR_OUT_OF_MEMORY if
+ * that fails) and held until the process ends.  Calls may come from several
+ * host threads, also on one stream: each call queues its two kernels
+ * without another call's kernels between them.
  */
 mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
                                      const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,

@@ -103,7 +103,10 @@ bool rows_aligned(const mla_tensor_t& t, int es) {
   return true;
 }
 
-// Split-K workspace: one grow-only buffer per (device, stream).
+// Split-K workspace: one grow-only buffer per (device, stream).  The caller
+// keeps `lock` (which holds g_ws_mutex) until both kernels that use the
+// buffer are queued, so that calls from several host threads on one stream
+// cannot queue a partial kernel between another call's partial and combine.
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
@@ -111,10 +114,11 @@ struct Workspace {
 std::mutex g_ws_mutex;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out) {
+mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out,
+                           std::unique_lock<std::mutex>& lock) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(MLA_ERR_HIP, "hipGetDevice failed");
-  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  lock = std::unique_lock<std::mutex>(g_ws_mutex);
   Workspace& ws = g_ws[{dev, stream}];
   if (ws.bytes < bytes) {
     if (ws.ptr) {
@@ -346,6 +350,7 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     p.out_s0 = out_lat->stride[0]; p.out_s1 = out_lat->stride[1]; p.out_s2 = out_lat->stride[2];
     p.lse = (float*)out_lse->data;
     p.lse_s0 = out_lse->stride[0]; p.lse_s1 = out_lse->stride[1]; p.lse_s2 = out_lse->stride[2];
+    std::unique_lock<std::mutex> ws_lock;  // held until the combine is queued
     if (S > 1) {
       // split rows, then their scales (fp16 rows only), then their lse values.
       // fp16 rows halve the workspace round trip, which pays once it moves
@@ -355,7 +360,8 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
       const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
       void* ws = nullptr;
-      if ((st = get_workspace(hs, o_bytes + 2 * n_part_rows * sizeof(float), &ws)) != MLA_OK) return st;
+      if ((st = get_workspace(hs, o_bytes + 2 * n_part_rows * sizeof(float), &ws, ws_lock)) != MLA_OK)
+        return st;
       p.ws_o32 = (float*)ws;
       p.ws_o16 = (uint16_t*)ws;
       p.ws_scale = (float*)((char*)ws + o_bytes);
