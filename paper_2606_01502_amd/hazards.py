@@ -30,6 +30,8 @@ import sys
 _REG = re.compile(r"\b([va])(?:(\d+)|\[(\d+):(\d+)\])")
 _LABEL = re.compile(r"^([.\w$]+):")
 _BRANCH = re.compile(r"^s_(?:cbranch_\w+|branch)\s+([.\w$]+)")
+# VALU instructions that write both of their register operands
+_WRITES_BOTH = ("v_swap_b32", "v_swap_b16", "v_permlane16_swap_b32", "v_permlane32_swap_b32")
 
 
 def _passes(op):
@@ -73,6 +75,8 @@ class Ins:
             if ops and _regs(ops[0]) and not op.startswith(("v_cmp", "v_cmpx")):
                 self.dst = _regs(ops[0])
                 self.src = _regs(" ".join(ops[1:]))
+                if op.startswith(_WRITES_BOTH) and len(ops) > 1:
+                    self.dst |= _regs(ops[1])
             else:
                 self.src = _regs(" ".join(ops))
         elif op.startswith(("ds_", "global_", "buffer_", "flat_", "scratch_")):

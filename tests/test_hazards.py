@@ -35,6 +35,14 @@ def test_valu_copy_right_before_asm_product():
     assert Z.check(_fn("\tv_add_u32_e32 v14, v40, v41\n" + _asm(MFMA)))
 
 
+def test_swaps_write_both_operands():
+    # the row-swap permutes (and v_swap) also write their second operand
+    for op in ("v_permlane16_swap_b32_e32", "v_permlane32_swap_b32_e32", "v_swap_b32"):
+        bad = Z.check(_fn(f"\t{op} v40, v6\n" + _asm(MFMA)))
+        assert bad and "has 0" in bad[0], op
+    assert Z.check(_fn("\tv_permlane16_swap_b32_e32 v40, v41\n" + _asm(MFMA))) == []
+
+
 def test_enough_wait_states_pass():
     assert Z.check(_fn("\tv_mov_b32_e32 v6, v40\n" + _asm("s_nop 1", MFMA))) == []
     assert Z.check(_fn("\tv_mov_b32_e32 v6, v40\n\ts_nop 0\n\tv_mov_b32_e32 v41, v40\n" +
