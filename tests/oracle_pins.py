@@ -157,6 +157,16 @@ def pin_bruteforce_per_row(lib):
     _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
 
 
+def pin_bruteforce_negative_scale(lib):
+    """Any finite scale is allowed: a negative one weights the lowest scores
+    most.  Brute force on a case with spread scores."""
+    import dataclasses
+    w = dataclasses.replace(W.random_case(14, R=2, Mq=2, H=2, P=7, NB=5, K=3, sigma=1.5),
+                            scale=-0.3)
+    out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, lib=lib)
+    _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
 def pin_per_row_is_one_job_per_row(lib):
     """Per-row selections equal the shared-selection form with every query
     row routed as a job of its own (Mq = 1) on the same chunk."""
@@ -496,4 +506,4 @@ ALL_PINS = [pin_bf16_decode, pin_e4m3_decode, pin_bruteforce_tiny, pin_bruteforc
             pin_bruteforce_fp8, pin_dense_equals_library, pin_identical_tokens,
             pin_identical_keys_mean, pin_zero_query, pin_two_groups, pin_one_hot,
             pin_empty_and_duplicates, pin_merge_partition, pin_merge_algebra,
-            pin_merge_zero_weight]
+            pin_merge_zero_weight, pin_bruteforce_negative_scale]

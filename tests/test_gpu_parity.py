@@ -99,6 +99,30 @@ def test_large_scale_near_one_hot():
     _check_case(w)
 
 
+@pytest.mark.parametrize("scale", [-0.07, 0.0])
+@pytest.mark.parametrize("kind", ["blocks", "tokens", "per_row", "fp8"])
+def test_nonpositive_scale(kind, scale):
+    """Any finite scale is allowed: a negative scale weights the lowest scores
+    most, and a zero scale gives every selected token the same weight."""
+    import dataclasses
+    print(f"case: scale={scale} kind={kind}", flush=True)
+    if kind == "tokens":
+        w = W.random_case(111, R=2, Mq=1, H=64, P=40, NB=30, K=100, tokens=True)
+    elif kind == "per_row":
+        w = W.random_case(112, R=2, Mq=3, H=16, P=20, NB=9, K=5, per_row=True)
+    else:
+        w = W.random_case(113, R=2, Mq=2, H=40, P=20, NB=9, K=7, sigma=2.0)
+        if kind == "fp8":
+            w = w.to_fp8(False)
+    w = dataclasses.replace(w, scale=scale)
+    t = G.upload(w)
+    for n_splits in (1, 3):
+        out, lse = G.run_partial(t, w.scale, n_splits=n_splits, tokens=kind == "tokens")
+        ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                                      w.ckv_scale, w.kpe_scale, tokens=kind == "tokens")
+        G.assert_parity(out, lse, ref_o, ref_l, f"{kind} scale={scale} splits={n_splits}")
+
+
 def test_zero_query_gives_mean():
     print("case: zero query", flush=True)
     w = W.random_case(107, R=1, Mq=1, H=16, P=6, NB=4, K=3)
