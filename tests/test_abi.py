@@ -4,6 +4,8 @@ import ctypes
 import os
 import re
 
+import pytest
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "mla_sparse.h")
 
@@ -71,7 +73,8 @@ def test_packed_descriptor_equals_fieldwise():
         assert bytes(mla.describe(t, bs)) == bytes(_describe_fieldwise(t, bs)), (t.shape, t.stride())
 
 
-def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0, tokens=False):
+def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0, tokens=False,
+              scale=0.1):
     """Call the partial entry point on CPU tensors: only the host-side checks
     run (each of these calls must fail before anything is launched)."""
     import types
@@ -87,7 +90,7 @@ def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0, toke
     sel = torch.zeros(sel_shape, dtype=torch.int32)
     stream = types.SimpleNamespace(cuda_stream=0)
     try:
-        mla.sparse_partial_attn(q_lat, q_pe, ckv, kpe, table, sel, 0.1, ckv_scale=sc,
+        mla.sparse_partial_attn(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=sc,
                                 kpe_scale=sc, row_tile=row_tile, stream=stream, tokens=tokens)
     except mla.MlaError as e:
         return e.status, str(e)
@@ -122,3 +125,17 @@ def test_row_tile_option_checked():
     for bad in (96, -64, 1, 256):
         st, msg = _cpu_call((2, 3), row_tile=bad)
         assert st == mla.MLA_ERR_INVALID_ARGUMENT and "row_tile" in msg
+
+
+def test_scale_must_be_finite():
+    """The last host check before planning and launch: shapes here are valid,
+    so only the scale stops these calls (negative and zero scales are
+    allowed and computed; see the GPU parity tests)."""
+    import torch
+    from paper_2606_01502_amd import mla
+    if torch.cuda.is_available():
+        pytest.skip("host-check test: its tensors live in host memory")
+    for bad in (float("inf"), float("-inf"), float("nan")):
+        for kw in ({}, {"tokens": True}, {"fp8": True}):
+            st, msg = _cpu_call((2, 3), scale=bad, **kw)
+            assert st == mla.MLA_ERR_INVALID_ARGUMENT and "scale" in msg, (bad, kw, msg)
