@@ -105,7 +105,9 @@ typedef struct {
  *                                     rows, or 64 when 128 would span more
  *                                     than 64 query rows) must not exceed
  *                                     73728 (MLA_ERR_UNSUPPORTED)
- *   scale                              multiplies q_lat.ckv + q_pe.kpe
+ *   scale                              multiplies q_lat.ckv + q_pe.kpe; any
+ *                                     finite value (0 weights every token
+ *                                     alike), else MLA_ERR_INVALID_ARGUMENT
  *   out_lat           [R, Mq, H, 512] fp32   written: normalised partial output
  *   out_lse           [R, Mq, H]      fp32   written: natural-log log-sum-exp
  *
