@@ -1,4 +1,4 @@
-"""Properties that hold without the oracle (the survey's invariant layer):
+"""Properties that hold without the oracle:
 the merge is commutative and has a zero-weight identity, the physical pool
 layout does not enter the arithmetic, and routing applies no rotation:
 re-homing a scattered selection at contiguous offsets (FETCH's splice, with
