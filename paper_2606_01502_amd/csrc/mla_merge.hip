@@ -164,7 +164,12 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
 
 __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineParams p) {
   const int n_rows = p.R * p.rows;
-  const int grow = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  // renumbered like the partial kernel (each XCD a contiguous range), so that
+  // a row tile's rows tend to be combined on the XCD whose L2 holds its
+  // splits' rows
+  const int blk = gridDim.x % 8 ? (int)blockIdx.x
+                               : (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
+  const int grow = blk * kRowsPerBlock + (threadIdx.x >> 6);
   if (grow >= n_rows) return;
   const int lane = threadIdx.x & 63;
   const int r = grow / p.rows;

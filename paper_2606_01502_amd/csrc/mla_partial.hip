@@ -804,8 +804,12 @@ void partial_kernel(const PartialParams p) {
   const int n16 = lane & 15;  // MFMA column / row-in-group index
   const int g = lane >> 4;    // MFMA k-group
 
-  // ---- work item
-  const int w_id = blockIdx.x;
+  // ---- work item.  Workgroups go to the 8 XCDs round-robin; the ids are
+  // renumbered so that each XCD takes one contiguous range.  The splits of a
+  // row tile then run on one XCD, and the combine, renumbered alike, reads
+  // their rows on that XCD when both grids split the rows alike.
+  const int w_id = gridDim.x % 8 ? (int)blockIdx.x
+                                 : (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
   const int s_idx = w_id % p.n_splits;
   const int rt = (w_id / p.n_splits) % p.row_tiles;
   const int r = w_id / (p.n_splits * p.row_tiles);
