@@ -51,7 +51,32 @@ def parse():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (untimed), a "
                          "known-size reference for hardware byte counters")
+    ap.add_argument("--cold-reps", type=int, default=-1,
+                    help="replica input sets for the cold-cache timing (-1: enough that the "
+                         "rotation touches more than 512 MiB, for workloads that touch less "
+                         "than 256 MiB per call; 0: skip)")
     return ap.parse_args()
+
+
+def stats_ms(durations):
+    """mean, p50 and min of per-step durations (ms)."""
+    d = np.asarray(durations, dtype=np.float64)
+    return {"mean": float(d.mean()), "p50": float(np.median(d)), "min": float(d.min())}
+
+
+def event_times(stream, fns, reps):
+    """Run fns[i % len(fns)] reps times back to back on `stream`, with a HIP
+    event recorded on that stream between consecutive calls; returns the
+    per-call durations in ms."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    stream.synchronize()
+    ev[0].record(stream)
+    for i in range(reps):
+        fns[i % len(fns)]()
+        ev[i + 1].record(stream)
+    stream.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]
 
 
 def code_fingerprint(path):
@@ -239,32 +264,65 @@ def main():
 
         K = args.steps
 
-        def timed(fn, reps):
-            """GPU time per call of fn, events recorded on the launch stream."""
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            stream.synchronize()
-            e0.record(stream)
-            for _ in range(reps):
-                fn()
-            e1.record(stream)
-            stream.synchronize()
-            return e0.elapsed_time(e1) / reps
-
-        # The timed region: K steps launched back to back on the stream.
+        # The timed region: K steps launched back to back on the stream, an
+        # event between consecutive steps (per-step p50 and min; the mean is
+        # the whole region over K).
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        step_ms = timed(lambda: (partial(), merge()), K)
+        step_d = event_times(stream, [lambda: (partial(), merge())], K)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        partial_ms = timed(partial, K)
-        merge_ms = timed(merge, K) if merged is not None else 0.0
+        partial_d = event_times(stream, [partial], K)
+        merge_d = event_times(stream, [merge], K) if merged is not None else [0.0]
         partial()
         merge()  # leave the outputs of one whole step in place
         torch.cuda.synchronize()
-    ms_step = step_ms
+    step_st, partial_st, merge_st = stats_ms(step_d), stats_ms(partial_d), stats_ms(merge_d)
+    ms_step = step_st["mean"]
+    partial_ms = partial_st["mean"]
+    merge_ms = merge_st["mean"]
 
+    # ---- cold caches: the same calls rotating over replica input sets (the
+    # same values at other addresses) that together touch more than 512 MiB,
+    # more than the 256 MiB last-level cache, so no call finds its inputs
+    # cached by the previous ones
     flops, alg_bytes, kv_bytes = algorithmic(w)
+    cold = None
+    n_rep = args.cold_reps
+    if n_rep < 0:
+        n_rep = (int((512 << 20) // max(alg_bytes, 1)) + 2) if alg_bytes < (256 << 20) else 0
+        n_rep = min(max(n_rep, 8), 4096) if n_rep else 0
+        pool_bytes = sum(v.numel() * v.element_size() for v in t.values() if v is not None)
+        n_rep = min(n_rep, int(32e9 // max(pool_bytes, 1)))  # replicas of every input
+    if n_rep > 0:
+        reps = []
+        for _ in range(n_rep):
+            rt = {k: (v.clone() if v is not None else None) for k, v in t.items()}
+            if t["ckv_scale"] is not None and t["kpe_scale"] is t["ckv_scale"]:
+                rt["kpe_scale"] = rt["ckv_scale"]
+            po = mla.prepare_partial(rt["q_lat"], rt["q_pe"], rt["ckv"], rt["kpe"], rt["table"],
+                                     rt["sel"], w.scale, out_lat, out_lse, rt["ckv_scale"],
+                                     rt["kpe_scale"], n_splits=args.n_splits, stream=stream,
+                                     tokens=w.tokens)
+            reps.append((rt, po))
+        calls = [r[1] for r in reps]
+        with torch.cuda.stream(stream):
+            for c in calls:
+                c()
+            stream.synchronize()
+            cold_d = event_times(stream, calls, max(K, 2 * n_rep))
+            step_cold_d = event_times(stream, [(lambda c=c: (c(), merge())) for c in calls],
+                                      max(K, 2 * n_rep))
+            partial()
+            merge()
+            torch.cuda.synchronize()
+        touched = n_rep * alg_bytes
+        cold = {"replicas": n_rep, "touched_mib": touched / 2 ** 20,
+                "partial_us": {k: v * 1e3 for k, v in stats_ms(cold_d).items()},
+                "step_us": {k: v * 1e3 for k, v in stats_ms(step_cold_d).items()},
+                "us_per_request_p50": stats_ms(step_cold_d)["p50"] * 1e3 / n_req}
+        del reps, calls
+
     part_s = partial_ms * 1e-3
     achieved = alg_bytes / part_s / 1e9
     tflops = flops / part_s / 1e12
@@ -313,6 +371,14 @@ def main():
                "kind": "oracle",
                "sample": f"{n} of {n_req} requests ({len(js)} of {R} partial jobs"
                          f"{' + their merge' if parts > 1 else ''}), fp64 C oracle"}
+        # the same oracle on one host thread, over one request (partials only)
+        js1, ri1 = jobs_of([0])
+        sel1 = w.sel[js1][:, ri1] if w.sel.ndim == 3 else w.sel[js1]
+        ts = time.perf_counter()
+        oracle.partial(w.q_lat[js1][:, ri1], w.q_pe[js1][:, ri1], w.ckv, w.kpe, w.table[js1], sel1,
+                       w.scale, w.ckv_scale, w.kpe_scale, tokens=w.tokens, n_threads=1)
+        cpu["value_1core"] = (time.perf_counter() - ts) * 1e6
+        cpu["sample_1core"] = "request 0 (its partial jobs), fp64 C oracle, 1 thread"
         rel = G.row_errors(out_np[js][:, ri].astype(np.float64), o_ref)
         lse_err = np.abs(lse_np[js][:, ri] - l_ref)
         parity = {"rows": int(rel.size), "max_row_rel_err": float(rel.max()),
@@ -335,6 +401,15 @@ def main():
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": achieved / HBM_PEAK_GBS, **common}
 
+    merge_roofline = None
+    if merged is not None:
+        m_rows = n_req * Mq * H
+        m_bytes = m_rows * (parts * (DLAT + 1) * 4 + DLAT * 4)  # parts + their lse in, rows out
+        m_ach = m_bytes / (merge_ms * 1e-3) / 1e9
+        m_traffic = counted_traffic(w.name, args.n_splits, "merge_kernel")
+        merge_roofline = {"bound": "hbm", "achieved": m_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": m_ach / HBM_PEAK_GBS, "traffic": m_traffic,
+                          "kernel": "merge_kernel", "algorithmic_bytes": m_bytes}
     res = {
         "metric": "us per routed request (sparse MLA partial attn + LSE merge)",
         "value": us_per_req,
@@ -356,6 +431,12 @@ def main():
         "pct_bf16_mfma_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
         "partial_kernel_us": partial_ms * 1e3,
         "merge_us": merge_ms * 1e3 if merged is not None else 0.0,
+        "step_us": {k: v * 1e3 for k, v in step_st.items()},
+        "partial_us": {k: v * 1e3 for k, v in partial_st.items()},
+        "merge_us_stats": ({k: v * 1e3 for k, v in merge_st.items()} if merged is not None
+                           else None),
+        "merge_roofline": merge_roofline,
+        "cold": cold,
         "host_wall_ms_per_step": (t1 - t0) * 1e3 / K,
         "roofline": roofline,
         "cpu_baseline": cpu,

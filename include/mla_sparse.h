@@ -29,9 +29,9 @@
  *     before anything is enqueued and write nothing; mla_last_error() then
  *     describes the problem.  No C++ exception crosses the ABI.
  *   - Device memory for split-K partials is allocated by the library on first
- *     need and reused (one grow-only buffer per device and stream, freed at
- *     unload).  Calls on different streams are independent; calls on one
- *     stream are ordered by the stream.
+ *     need and reused (one grow-only buffer per device and stream; see
+ *     "Split-K workspace" below).  Calls on different streams are
+ *     independent; calls on one stream are ordered by the stream.
  */
 #ifndef MLA_SPARSE_H
 #define MLA_SPARSE_H
@@ -91,7 +91,16 @@ typedef struct {
  *                                     passing the same array for both (one scale
  *                                     per block for the whole 576-wide entry) is
  *                                     the fast layout, two arrays (separate
- *                                     latent and RoPE scales) are also accepted
+ *                                     latent and RoPE scales) are also accepted.
+ *                                     Scales must be finite; 0 is allowed (the
+ *                                     block's values are then 0).  With two
+ *                                     arrays, a block whose latent scale is 0 or
+ *                                     below 2^-64 of its RoPE scale has its
+ *                                     latent score part weighted by 2^-64 times
+ *                                     the RoPE scale instead (an absolute score
+ *                                     error of at most 2^-63 |RoPE scale| |q_lat .
+ *                                     latent codes|); its values keep the latent
+ *                                     scale.
  *   chunk_block_table [R, NB] int32   logical block of job r's chunk -> pool block
  *   sel_block_ids     [R, K]  int32   selected logical blocks; -1 marks an empty
  *                                     slot; a block listed twice counts twice
@@ -104,10 +113,15 @@ typedef struct {
  *                                     the query rows one row tile spans (128
  *                                     rows, or 64 when 128 would span more
  *                                     than 64 query rows) must not exceed
- *                                     73728 (MLA_ERR_UNSUPPORTED)
- *   scale                              multiplies q_lat.ckv + q_pe.kpe; any
- *                                     finite value (0 weights every token
- *                                     alike), else MLA_ERR_INVALID_ARGUMENT
+ *                                     73696 (MLA_ERR_UNSUPPORTED)
+ *   scale                              multiplies q_lat.ckv + q_pe.kpe: any
+ *                                     value with |scale| <= 2^64 (0 weights
+ *                                     every token alike), else
+ *                                     MLA_ERR_INVALID_ARGUMENT.  Scores are
+ *                                     formed in fp32: the result is defined
+ *                                     while |q_lat.ckv + q_pe.kpe| < 2^63 for
+ *                                     every selected token (bf16 products
+ *                                     accumulated in fp32)
  *   out_lat           [R, Mq, H, 512] fp32   written: normalised partial output
  *   out_lse           [R, Mq, H]      fp32   written: natural-log log-sum-exp
  *
@@ -124,11 +138,20 @@ typedef struct {
  * does not detect on the host: such a slot is skipped (treated as empty).
  *
  * Split-K workspace: when a job is split, the library keeps one grow-only
- * device buffer per (device, stream), allocated on first need (a larger
- * need synchronizes the stream and reallocates; MLA_ERR_OUT_OF_MEMORY if
- * that fails) and held until the process ends.  Calls may come from several
- * host threads, also on one stream: each call queues its two kernels
- * without another call's kernels between them.
+ * device buffer per (device, stream), allocated on first need
+ * (MLA_ERR_OUT_OF_MEMORY if that fails).  A larger need allocates a new
+ * buffer of at least twice the size; the old one is kept, not freed, until
+ * the process ends, so a HIP graph captured with it stays valid.  Calls may
+ * come from several host threads, also on one stream: each call queues its
+ * two kernels without another call's kernels between them.
+ * Graph capture: a call captured on a stream uses that stream's workspace
+ * as it was at capture time.  The workspace cannot grow while the stream is
+ * being captured (MLA_ERR_UNSUPPORTED): make the same call, or a larger one,
+ * on the stream before capturing.  Replay the graph on the stream it was
+ * captured on, or keep other calls on that stream from running at the same
+ * time as the replay (they share the buffer).  Under global-mode capture,
+ * a call on another stream that has to grow its workspace allocates device
+ * memory, which that capture mode forbids.
  */
 mla_status_t mla_sparse_partial_attn(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
                                      const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,

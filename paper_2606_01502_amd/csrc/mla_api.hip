@@ -11,6 +11,7 @@
 #include <mutex>
 #include <string>
 #include <utility>
+#include <vector>
 
 #include "../../include/mla_sparse.h"
 #include "mla_kernels.h"
@@ -107,12 +108,21 @@ bool rows_aligned(const mla_tensor_t& t, int es) {
 // keeps `lock` (which holds g_ws_mutex) until both kernels that use the
 // buffer are queued, so that calls from several host threads on one stream
 // cannot queue a partial kernel between another call's partial and combine.
+//
+// A buffer is never freed while the process runs: a HIP graph captured on the
+// stream keeps the address it was captured with, and replaying it after a
+// larger call has replaced the buffer must still find that memory.  Replaced
+// buffers are retired (kept), and each replacement at least doubles the size,
+// so the retired ones together stay below the live one.  Growing is refused
+// while the stream is being captured (an allocation there is not part of the
+// graph, and under global capture it would invalidate the capture).
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
 };
 std::mutex g_ws_mutex;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::vector<void*> g_ws_retired;
 
 mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out,
                            std::unique_lock<std::mutex>& lock) {
@@ -121,19 +131,25 @@ mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out,
   lock = std::unique_lock<std::mutex>(g_ws_mutex);
   Workspace& ws = g_ws[{dev, stream}];
   if (ws.bytes < bytes) {
-    if (ws.ptr) {
-      // the previous buffer may still be in use by work queued on this stream
-      if (hipStreamSynchronize(stream) != hipSuccess) return fail(MLA_ERR_HIP, "hipStreamSynchronize failed");
-      (void)hipFree(ws.ptr);
-      ws.ptr = nullptr;
-      ws.bytes = 0;
-    }
-    const size_t want = std::max(bytes, (size_t)1 << 20);
-    if (hipMalloc(&ws.ptr, want) != hipSuccess) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cap) != hipSuccess) {
       (void)hipGetLastError();
-      ws.ptr = nullptr;
+      return fail(MLA_ERR_HIP, "hipStreamIsCapturing failed");
+    }
+    if (cap != hipStreamCaptureStatusNone)
+      return fail(MLA_ERR_UNSUPPORTED,
+                  "the split-K workspace of this stream (" + std::to_string(ws.bytes) +
+                      " bytes) is smaller than this call needs (" + std::to_string(bytes) +
+                      ") and cannot grow during stream capture: make the call once on this "
+                      "stream before capturing it");
+    const size_t want = std::max({bytes, 2 * ws.bytes, (size_t)1 << 20});
+    void* fresh = nullptr;
+    if (hipMalloc(&fresh, want) != hipSuccess) {
+      (void)hipGetLastError();
       return fail(MLA_ERR_OUT_OF_MEMORY, "split-K workspace allocation of " + std::to_string(want) + " bytes failed");
     }
+    if (ws.ptr) g_ws_retired.push_back(ws.ptr);  // may still be in a captured graph
+    ws.ptr = fresh;
     ws.bytes = want;
   }
   *out = ws.ptr;
@@ -216,7 +232,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     if (!rows_aligned(*q_lat, 2) || !rows_aligned(*q_pe, 2))
       return fail(MLA_ERR_INVALID_ARGUMENT, "q_lat/q_pe rows must be 16-byte aligned");
     if (!rows_aligned(*out_lat, 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat rows must be 16-byte aligned");
-    if (!std::isfinite(scale)) return fail(MLA_ERR_INVALID_ARGUMENT, "scale must be finite");
+    // |scale| <= 2^64 keeps scale * log2(e) and the scores of any bf16 or fp8
+    // rows whose dot products stay below 2^63 finite in fp32
+    if (!(std::fabs(scale) <= 18446744073709551616.0f))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "scale must be finite with |scale| <= 2^64");
     if (R > INT32_MAX || Mq * H > (1 << 24) || K > INT32_MAX || NB > INT32_MAX || P > INT32_MAX)
       return fail(MLA_ERR_UNSUPPORTED, "sizes beyond the int32 index range");
     if (tokens && (NB > (INT32_MAX >> 6) || P > (INT32_MAX >> 6)))

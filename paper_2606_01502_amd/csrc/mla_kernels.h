@@ -110,7 +110,7 @@ constexpr int kKvFp8Split = 2;   // e4m3, separate ckv and kpe scales per block
 
 // Per-row selections: the LDS counters of one workgroup's compaction live in
 // its stage area, NB * (query rows of the tile) 16-bit counters.
-constexpr int kPerRowCounterBytes = 2 * 64 * 1152;  // the bf16 stage area
+constexpr int kPerRowCounterBytes = 2 * 64 * 1152 - 64;  // the stage area, less the wave counters
 constexpr int kPerRowMaxRows = 64;                  // query rows per row tile (mask bits)
 constexpr int kPerRowListFp8 = kMaxSlotsPerSplit / 2;  // list entries per split, fp8 caches
 

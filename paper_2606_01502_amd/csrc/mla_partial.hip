@@ -76,8 +76,9 @@ typedef int i32x2_t __attribute__((ext_vector_type(2)));
 // one block of e4m3 codes each (64 latent rows of 512 B, then 64 RoPE rows of
 // 64 B, swizzled as described at fp8_key); blocks h+1 .. h+3 stream in while
 // block h is computed.  After the stages: the compacted pool-block list of
-// the slot range and, for fp8, two floats per listed block (latent scale,
-// RoPE / latent scale ratio).
+// the slot range and, for fp8, three floats per listed block (see
+// fp8_factors).  The compactions' per-wave counters use the last bytes of the
+// stage area, which no load writes before the compaction is over.
 template <bool FP8>
 struct Layout {
   static constexpr int kElt = FP8 ? 1 : 2;                     // bytes per element
@@ -90,22 +91,22 @@ struct Layout {
   static constexpr int kLoads = kStage / 1024 / 4;  // 1 KiB loads per wave per stage
   static constexpr int kList = kNum * kStage;
   static constexpr int kScales = kList + kMaxSlotsPerSplit * 4;
-  static constexpr int kWaveCnt = kScales + (FP8 ? kMaxSlotsPerSplit * 8 : 0);
-  static constexpr int kTotal = kWaveCnt + 16;
+  static constexpr int kTotal = kScales + (FP8 ? kMaxSlotsPerSplit * 12 : 0);
+  static constexpr int kWaveCnt = kNum * kStage - 16;
   // Per-row selections: a 64-bit row mask per list entry.  bf16: after the
   // rest, for a full list.  fp8 (whose four stages leave no room for that):
   // half a list, its scales and masks sharing the scale area.
   static constexpr int kPerRowCap = FP8 ? kMaxSlotsPerSplit / 2 : kMaxSlotsPerSplit;
-  static constexpr int kMasks = FP8 ? kScales + kPerRowCap * 8 : kTotal;
+  static constexpr int kMasks = FP8 ? kScales + kPerRowCap * 12 : kTotal;
   static constexpr int kTotalPerRow = FP8 ? kTotal : kMasks + kPerRowCap * 8;
 };
-static_assert(Layout<true>::kMasks + Layout<true>::kPerRowCap * 8 <= Layout<true>::kWaveCnt,
+static_assert(Layout<true>::kMasks + Layout<true>::kPerRowCap * 8 <= Layout<true>::kTotal,
               "fp8 per-row scales and masks fit the scale area");
 static_assert(Layout<true>::kPerRowCap == kPerRowListFp8, "per-row fp8 list size");
 static_assert(Layout<true>::kTotal <= 160 * 1024 && Layout<false>::kTotalPerRow <= 160 * 1024,
               "LDS budget");
-static_assert(kPerRowCounterBytes <= Layout<false>::kNum * Layout<false>::kStage,
-              "per-row counters live in the stage area");
+static_assert(kPerRowCounterBytes <= Layout<false>::kWaveCnt && kPerRowCounterBytes <= Layout<true>::kWaveCnt,
+              "per-row counters live in the stage area, below the wave counters");
 constexpr float kTau = 8.0f;        // lazy-rescale threshold, log2 units
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -578,9 +579,39 @@ struct VFrags8 {
   }
 };
 
+// The score factors of an fp8 block with latent scale sc and RoPE scale sk.
+// Its scores are scale * (sc * (q_lat . latent codes) + sk * (q_pe . RoPE
+// codes)); the kernel forms them as main * (q_lat . latent codes + ratio *
+// (q_pe . RoPE codes)), one accumulator for both parts.  While |sk| < 2^64 |sc|
+// that is exact: main = sc, ratio = sk / sc.  Otherwise (a latent scale of 0,
+// or one below 2^-64 of the RoPE scale) main = sk * 2^-64 and ratio = 2^64:
+// the score then differs from the exact one by (sk 2^-64 - sc)(q_lat . codes),
+// at most 2^-63 |sk| |q_lat . codes|, and nothing is divided by zero.  The
+// values themselves always take the latent scale sc.
+__device__ __forceinline__ void fp8_factors(float sc, float sk, float& main, float& ratio) {
+  constexpr float kBig = 18446744073709551616.0f;  // 2^64
+  if (fabsf(sk) < kBig * fabsf(sc)) {
+    main = sc;
+    ratio = sk / sc;
+  } else {
+    main = sk * (1.0f / kBig);
+    ratio = kBig;
+  }
+}
+
+// Per-listed-block fp8 factors in LDS: [3 i] value scale, [3 i + 1] score
+// factor main, [3 i + 2] RoPE ratio (see fp8_factors).
+__device__ __forceinline__ void put_fp8_factors(LDS float* scales, int i, float sc, float sk) {
+  float main, ratio;
+  fp8_factors(sc, sk, main, ratio);
+  scales[3 * i] = sc;
+  scales[3 * i + 1] = main;
+  scales[3 * i + 2] = ratio;
+}
+
 // Compact the valid selected blocks of slots [slot0, slot0 + nslots) of job r
-// into the LDS list (slot order kept); for fp8 also each listed block's latent
-// scale and RoPE / latent scale ratio.  Returns the number of listed blocks.
+// into the LDS list (slot order kept); for fp8 also each listed block's
+// factors (put_fp8_factors).  Returns the number of listed blocks.
 template <bool FP8>
 __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int slot0, int nslots,
                                              LDS uint8_t* smem, int tid) {
@@ -614,11 +645,7 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
     }
     if (b >= 0) {
       list[off + before] = b;
-      if constexpr (FP8) {
-        const float sc = p.ckv_scale[b];
-        scales[2 * (off + before)] = sc;
-        scales[2 * (off + before) + 1] = p.kpe_scale[b] / sc;
-      }
+      if constexpr (FP8) put_fp8_factors(scales, off + before, p.ckv_scale[b], p.kpe_scale[b]);
     }
     n_valid += total;
     lds_barrier();
@@ -636,7 +663,7 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
 // come in ascending logical-block order.  The counters (16 bits per (block,
 // row) of the blocks taken; at most nslots each) use the stage area, which is
 // free until the first load is issued.  Returns the number of entries.
-// fp8: each entry also gets its block's latent scale and RoPE / latent ratio.
+// fp8: each entry also gets its block's factors (put_fp8_factors).
 template <bool FP8>
 __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, int slot0,
                                                int nslots, int id0, int id_step, int i0, int n_i,
@@ -690,10 +717,10 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
     }
     if (kmax > 0) {
       const int bb = p.table[r * p.table_s0 + id];
-      float sc = 1.f, ratio = 1.f;
+      float sc = 1.f, sk = 1.f;
       if constexpr (FP8) {
         sc = p.ckv_scale[bb];
-        ratio = p.kpe_scale[bb] / sc;
+        sk = p.kpe_scale[bb];
       }
       for (int k = 0; k < kmax; ++k) {
         uint64_t m = 0;
@@ -701,10 +728,7 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
           if ((int)cnt16[u * n_i + ii] > k) m |= 1ull << ii;
         list[off + k] = bb;
         masks[off + k] = m;
-        if constexpr (FP8) {
-          scales[2 * (off + k)] = sc;
-          scales[2 * (off + k) + 1] = ratio;
-        }
+        if constexpr (FP8) put_fp8_factors(scales, off + k, sc, sk);
       }
     }
     n_valid += total;
@@ -717,10 +741,11 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
 // nslots) of job r into the LDS list as pool tokens (table[r, id / 64] * 64 +
 // id % 64), slot order kept, and fill the list up to the next multiple of 64
 // with the first entry, so that the last virtual block loads only listed
-// tokens (the fill is masked out of the softmax).  fp8: entry i's latent
-// scale goes to tok_scales[i] and its RoPE / latent scale ratio to
-// tok_scales[kMaxSlotsPerSplit + i] (each token carries its own block's
-// scales).  Returns the number of listed tokens.
+// tokens (the fill is masked out of the softmax).  fp8: each token carries
+// its own block's factors (fp8_factors): the value scale in tok_scales[i],
+// the RoPE ratio in tok_scales[kMaxSlotsPerSplit + i] and the score factor
+// in tok_scales[2 kMaxSlotsPerSplit + i].  Returns the number of listed
+// tokens.
 template <bool FP8>
 __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int slot0,
                                               int nslots, LDS uint8_t* smem, int tid) {
@@ -758,8 +783,11 @@ __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int
       if constexpr (FP8) {
         const int bb = pt >> 6;
         const float sc = p.ckv_scale[bb];
+        float main, ratio;
+        fp8_factors(sc, p.kpe_scale[bb], main, ratio);
         tok_scales[off + before] = sc;
-        tok_scales[kMaxSlotsPerSplit + off + before] = p.kpe_scale[bb] / sc;
+        tok_scales[kMaxSlotsPerSplit + off + before] = ratio;
+        tok_scales[2 * kMaxSlotsPerSplit + off + before] = main;
       }
     }
     n_tok += total;
@@ -772,6 +800,7 @@ __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int
       if constexpr (FP8) {
         tok_scales[i] = tok_scales[0];
         tok_scales[kMaxSlotsPerSplit + i] = tok_scales[kMaxSlotsPerSplit];
+        tok_scales[2 * kMaxSlotsPerSplit + i] = tok_scales[2 * kMaxSlotsPerSplit];
       }
     }
   }
@@ -929,14 +958,14 @@ void partial_kernel(const PartialParams p) {
     }
     __builtin_amdgcn_sched_barrier(0);
     // fp8: the scores are accumulated as ratio * (q_pe . kpe codes) +
-    // q_lat . ckv codes (ratio = RoPE scale / latent scale) and then scaled by
-    // the softmax scale times the latent scale; P is scaled by the latent
-    // scale before its bf16 rounding.
+    // q_lat . ckv codes and then scaled by the softmax scale times the
+    // block's score factor (fp8_factors); P is scaled by the latent scale
+    // before its bf16 rounding.
     float s_mult = p.scale_log2, v_mult = 1.f, pe_ratio = 1.f;
     if constexpr (FP8 && !TOK) {
-      v_mult = scales[2 * h];
-      if constexpr (kSplitScales) pe_ratio = scales[2 * h + 1];
-      s_mult = p.scale_log2 * v_mult;
+      v_mult = scales[3 * h];
+      if constexpr (kSplitScales) pe_ratio = scales[3 * h + 2];
+      s_mult = p.scale_log2 * scales[3 * h + 1];
     }
     const LDS uint8_t* const cb = stage0 + (h % L::kNum) * L::kStage;
     // The next stage's loads.  bf16: two per S^T step over the first nine
@@ -1167,7 +1196,7 @@ void partial_kernel(const PartialParams p) {
       float bm = -INFINITY;
 #pragma unroll
       for (int tau = 0; tau < kTau4; ++tau) {
-        if constexpr (FP8 && TOK) acc[rg][tau] *= tok_scale4(0, tau) * s_mult;
+        if constexpr (FP8 && TOK) acc[rg][tau] *= tok_scale4(2, tau) * s_mult;
         else acc[rg][tau] *= s_mult;
         if (TOK && n_here < kBlock) {
 #pragma unroll

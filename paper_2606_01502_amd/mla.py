@@ -153,6 +153,18 @@ def describe(t: torch.Tensor | None, block_scale: torch.Tensor | None = None) ->
                                               *stride, *pad, bs))
 
 
+def _on_one_gpu(*tensors):
+    """Raise ValueError unless every given tensor lives on one CUDA (HIP)
+    device: the library reads and writes device memory only, and a host
+    tensor's address handed to a kernel would fault."""
+    devs = {t.device for t in tensors if t is not None}
+    bad = [d for d in devs if d.type != "cuda"]
+    if bad:
+        raise ValueError(f"tensors must be on the GPU, got {bad[0]}")
+    if len(devs) > 1:
+        raise ValueError(f"tensors must be on one device, got {sorted(map(str, devs))}")
+
+
 def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -190,6 +202,8 @@ def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_
         out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
     if out_lse is None:
         out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
+    _on_one_gpu(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, out_lat,
+                out_lse, ckv_scale, kpe_scale)
     opts = PartialOpts()
     opts.n_splits = int(n_splits)
     opts.row_tile = int(row_tile)
@@ -246,6 +260,7 @@ def fetch_gather(ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, out_ckv=N
         out_ckv = torch.empty((L, K, DLAT), dtype=torch.bfloat16, device=ckv_pool.device)
     if out_kpe is None:
         out_kpe = torch.empty((L, K, DPE), dtype=torch.bfloat16, device=ckv_pool.device)
+    _on_one_gpu(ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, out_ckv, out_kpe)
     lib = load()
     d = [describe(t) for t in (ckv_pool, kpe_pool, chunk_block_table, sel_token_ids, out_ckv,
                                out_kpe)]
@@ -259,6 +274,7 @@ def fetch_splice(chunk_ckv, chunk_kpe, ckv_pool, kpe_pool, block_table, dst_star
     paged pools at positions dst_start .. dst_start + n - 1 of the sequence
     that block_table maps, its RoPE pairs turned by delta positions
     (pairing 0: dims (2i, 2i+1), 1: dims (i, i+32))."""
+    _on_one_gpu(chunk_ckv, chunk_kpe, ckv_pool, kpe_pool, block_table)
     lib = load()
     d = [describe(t) for t in (chunk_ckv, chunk_kpe, ckv_pool, kpe_pool, block_table)]
     _check(lib, lib.mla_fetch_splice(*[_ref(x) for x in d], int(dst_start), int(delta),
@@ -289,6 +305,7 @@ def _merge_args(parts_lat, parts_lse, out, out_lse, stream):
         out = torch.empty_like(parts_lat[0])
     if out_lse is True:
         out_lse = torch.empty_like(parts_lse[0])
+    _on_one_gpu(*parts_lat, *parts_lse, out, out_lse if want_lse else None)
     d_lat = [describe(t) for t in parts_lat]
     d_lse = [describe(t) for t in parts_lse]
     arr_lat = (ctypes.POINTER(Tensor) * max(n, 1))(*[ctypes.pointer(d) for d in d_lat])

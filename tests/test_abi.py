@@ -75,26 +75,17 @@ def test_packed_descriptor_equals_fieldwise():
 
 def _cpu_call(sel_shape, fp8=False, R=2, Mq=3, H=16, P=8, NB=5, row_tile=0, tokens=False,
               scale=0.1):
-    """Call the partial entry point on CPU tensors: only the host-side checks
-    run (each of these calls must fail before anything is launched)."""
-    import types
+    """Call the partial entry point on host tensors through ctypes: only the
+    host-side checks run (each of these calls must fail before anything is
+    launched)."""
     import torch
-    from paper_2606_01502_amd import mla
-    kv = torch.uint8 if fp8 else torch.bfloat16
-    q_lat = torch.zeros((R, Mq, H, 512), dtype=torch.bfloat16)
-    q_pe = torch.zeros((R, Mq, H, 64), dtype=torch.bfloat16)
-    ckv = torch.zeros((P, 64, 512), dtype=kv)
-    kpe = torch.zeros((P, 64, 64), dtype=kv)
-    sc = torch.ones(P, dtype=torch.float32) if fp8 else None
-    table = torch.zeros((R, NB), dtype=torch.int32)
-    sel = torch.zeros(sel_shape, dtype=torch.int32)
-    stream = types.SimpleNamespace(cuda_stream=0)
-    try:
-        mla.sparse_partial_attn(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=sc,
-                                kpe_scale=sc, row_tile=row_tile, stream=stream, tokens=tokens)
-    except mla.MlaError as e:
-        return e.status, str(e)
-    return mla.MLA_OK, ""
+    from tests import abi_cases as C
+    a = C.partial_args(torch.device("cpu"), fp8=fp8, R=R, Mq=Mq, H=H, P=P, NB=NB)
+    a["sel"] = torch.zeros(sel_shape, dtype=torch.int32)
+    a["opts"].row_tile = row_tile
+    a["tokens"] = tokens
+    a["scale"] = scale
+    return C.call_partial(a)
 
 
 def test_per_row_selection_host_checks():
@@ -127,7 +118,7 @@ def test_row_tile_option_checked():
         assert st == mla.MLA_ERR_INVALID_ARGUMENT and "row_tile" in msg
 
 
-def test_scale_must_be_finite():
+def test_scale_must_be_finite_and_bounded():
     """The last host check before planning and launch: shapes here are valid,
     so only the scale stops these calls (negative and zero scales are
     allowed and computed; see the GPU parity tests)."""
@@ -135,7 +126,7 @@ def test_scale_must_be_finite():
     from paper_2606_01502_amd import mla
     if torch.cuda.is_available():
         pytest.skip("host-check test: its tensors live in host memory")
-    for bad in (float("inf"), float("-inf"), float("nan")):
+    for bad in (float("inf"), float("-inf"), float("nan"), 2.0 ** 64 * (1 + 2.0 ** -23), -(2.0 ** 70)):
         for kw in ({}, {"tokens": True}, {"fp8": True}):
             st, msg = _cpu_call((2, 3), scale=bad, **kw)
             assert st == mla.MLA_ERR_INVALID_ARGUMENT and "scale" in msg, (bad, kw, msg)

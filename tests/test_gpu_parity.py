@@ -224,3 +224,18 @@ def test_strided_queries_and_outputs(n_splits, tokens):
         w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, tokens=True)
     G.assert_parity(out_v.cpu().numpy().astype(np.float64), lse_v.cpu().numpy().astype(np.float64),
                     o_or, l_or, "strided")
+
+
+def test_dense_local_bf16_config_sampled():
+    """The dense-local workload with a bf16 cache at full size (32 jobs x 1024
+    blocks x 128 heads, each job attending all 65,536 tokens of its chunk,
+    the dense holder of Section 6.3): every job on the GPU with the library's
+    plan (128-row tiles, long splits, the scaled-fp16 split workspace), three
+    jobs on the oracle."""
+    print("case: dense-local bf16 sampled", flush=True)
+    w = W.make("dense-local")
+    jobs = [0, 17, 31]
+    out, lse = G.run_partial(G.upload(w), w.scale)
+    ref_o, ref_l = _oracle(w, jobs)
+    rel, lerr = G.assert_parity(out[jobs], lse[jobs], ref_o, ref_l, "dense-local bf16")
+    print(f"dense-local bf16: max row-rel {rel:.3g}, max lse {lerr:.3g}", flush=True)
