@@ -185,6 +185,34 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
                                         const mla_partial_opts_t* opts, void* stream);
 
 /*
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that
+ * forbid allocation.  mla_sparse_partial_attn_ex with the same arguments,
+ * layout rules, result and errors, except that its split-K workspace is a
+ * static device array of MLA_NOALLOC_SCRATCH_BYTES (64 MiB) that the library
+ * holds on each GPU it runs on until the process ends, instead of memory it
+ * allocates.  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).  A call whose split partials need more than the array (about
+ * 32K partial rows: jobs x row tiles x splits x 128 rows) returns
+ * MLA_ERR_UNSUPPORTED before anything is enqueued.  Every call on one GPU
+ * shares that GPU's array: calls that overlap in time on one GPU (on
+ * different streams, or from graphs replayed concurrently) race on it and
+ * must be ordered by the caller; calls on one stream are ordered by the
+ * stream.  Nothing in the array needs clearing between calls (each call
+ * writes every workspace entry it reads).
+ */
+#define MLA_NOALLOC_SCRATCH_BYTES (64ll << 20)
+mla_status_t mla_sparse_partial_attn_noalloc(const mla_tensor_t* q_lat,
+                                             const mla_tensor_t* q_pe,
+                                             const mla_tensor_t* ckv_pool,
+                                             const mla_tensor_t* kpe_pool,
+                                             const mla_tensor_t* chunk_block_table,
+                                             const mla_tensor_t* sel_block_ids, float scale,
+                                             const mla_tensor_t* out_lat,
+                                             const mla_tensor_t* out_lse,
+                                             const mla_partial_opts_t* opts, void* stream);
+
+/*
  * The same partial attention over single selected tokens: an indexer's top-k
  * tokens of the chunk (the selection budgets of Section 6.3, k = 512 .. 2048
  * attended entries) rather than whole 64-token blocks.

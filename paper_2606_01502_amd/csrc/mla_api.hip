@@ -156,6 +156,36 @@ mla_status_t get_workspace(hipStream_t stream, size_t bytes, void** out,
   return MLA_OK;
 }
 
+// The split-K workspace of mla_sparse_partial_attn_noalloc: a static device
+// array that the runtime places on every GPU the library runs on, held until
+// the process ends.  Host code never uses its name as an address (on the host
+// it names a stand-in); each device's address comes from hipGetSymbolAddress,
+// taken once per device on the first call there, with that device current.
+static __device__ __align__(256) uint8_t scratch[MLA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+mla_status_t scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(MLA_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MLA_ERR_UNSUPPORTED, "device index beyond 64");
+  std::lock_guard<std::mutex> guard(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return fail(MLA_ERR_HIP, std::string("hipGetSymbolAddress of the scratch array: ") +
+                                   hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return MLA_OK;
+}
+
 int device_cus() {
   static int cus = 0;
   if (cus == 0) {
@@ -170,13 +200,15 @@ int device_cus() {
 }
 
 // The partial call; `tokens`: sel names single logical tokens (block * 64 +
-// t) rather than blocks.
+// t) rather than blocks; `no_alloc`: the split-K workspace is the static
+// scratch array (nothing is allocated; sizes beyond it are refused).
 mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
                           const mla_tensor_t* ckv_pool, const mla_tensor_t* kpe_pool,
                           const mla_tensor_t* chunk_block_table,
                           const mla_tensor_t* sel_block_ids, float scale,
                           const mla_tensor_t* out_lat, const mla_tensor_t* out_lse,
-                          const mla_partial_opts_t* opts, void* stream, bool tokens) {
+                          const mla_partial_opts_t* opts, void* stream, bool tokens,
+                          bool no_alloc = false) {
   try {
     g_last_error.clear();
     mla_status_t st;
@@ -378,9 +410,19 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       const size_t n_part_rows = (size_t)R * S * rows;
       p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
       const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
+      const size_t ws_bytes = o_bytes + 2 * n_part_rows * sizeof(float);
       void* ws = nullptr;
-      if ((st = get_workspace(hs, o_bytes + 2 * n_part_rows * sizeof(float), &ws, ws_lock)) != MLA_OK)
+      if (no_alloc) {
+        if (ws_bytes > (size_t)MLA_NOALLOC_SCRATCH_BYTES)
+          return fail(MLA_ERR_UNSUPPORTED,
+                      "this call's split-K partials need " + std::to_string(ws_bytes) +
+                          " bytes, more than the " + std::to_string((long long)MLA_NOALLOC_SCRATCH_BYTES) +
+                          "-byte scratch array of the allocation-free entry point (fewer jobs or "
+                          "splits per call)");
+        if ((st = scratch_address(&ws)) != MLA_OK) return st;
+      } else if ((st = get_workspace(hs, ws_bytes, &ws, ws_lock)) != MLA_OK) {
         return st;
+      }
       p.ws_o32 = (float*)ws;
       p.ws_o16 = (uint16_t*)ws;
       p.ws_scale = (float*)((char*)ws + o_bytes);
@@ -427,6 +469,18 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
                                         const mla_partial_opts_t* opts, void* stream) {
   return partial_call(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                       out_lat, out_lse, opts, stream, false);
+}
+
+mla_status_t mla_sparse_partial_attn_noalloc(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
+                                             const mla_tensor_t* ckv_pool,
+                                             const mla_tensor_t* kpe_pool,
+                                             const mla_tensor_t* chunk_block_table,
+                                             const mla_tensor_t* sel_block_ids, float scale,
+                                             const mla_tensor_t* out_lat,
+                                             const mla_tensor_t* out_lse,
+                                             const mla_partial_opts_t* opts, void* stream) {
+  return partial_call(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
+                      out_lat, out_lse, opts, stream, false, true);
 }
 
 mla_status_t mla_sparse_partial_attn_tokens(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,

@@ -28,7 +28,7 @@ DTYPE_BF16, DTYPE_FP8_E4M3FN, DTYPE_FP32, DTYPE_INT32 = 1, 2, 3, 4
 EXPORTS = ("mla_sparse_partial_attn", "mla_sparse_partial_attn_ex",
            "mla_sparse_partial_attn_tokens", "mla_merge_partials", "mla_merge_partials_ex",
            "mla_last_error", "mla_version", "mla_primitive_costs", "mla_fetch_gather",
-           "mla_fetch_splice")
+           "mla_fetch_splice", "mla_sparse_partial_attn_noalloc")
 
 
 class MlaError(RuntimeError):
@@ -97,6 +97,8 @@ def load(path: str = LIB_PATH):
                                                ctypes.POINTER(PartialOpts), vp]
     lib.mla_sparse_partial_attn_tokens.restype = ctypes.c_int
     lib.mla_sparse_partial_attn_tokens.argtypes = lib.mla_sparse_partial_attn_ex.argtypes
+    lib.mla_sparse_partial_attn_noalloc.restype = ctypes.c_int
+    lib.mla_sparse_partial_attn_noalloc.argtypes = lib.mla_sparse_partial_attn_ex.argtypes
     lib.mla_merge_partials.restype = ctypes.c_int
     lib.mla_merge_partials.argtypes = [PP, PP, ctypes.c_int32, P, vp]
     lib.mla_merge_partials_ex.restype = ctypes.c_int
@@ -217,9 +219,17 @@ def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_
     return args, keep, (out_lat, out_lse)
 
 
+def _partial_fn(lib, tokens, no_alloc):
+    if tokens and no_alloc:
+        raise ValueError("the allocation-free entry point takes block selections only")
+    if no_alloc:
+        return lib.mla_sparse_partial_attn_noalloc
+    return lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
+
+
 def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                     out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None, n_splits=0,
-                    row_tile=0, stream=None, tokens=False):
+                    row_tile=0, stream=None, tokens=False, no_alloc=False):
     """sparse_partial_attn with every argument fixed, the stream included
     (the current one when None); calling the result launches the work and
     returns (out_lat, out_lse)."""
@@ -227,16 +237,17 @@ def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_bloc
                                        sel_block_ids, scale, out_lat, out_lse, ckv_scale,
                                        kpe_scale, n_splits, row_tile, stream)
     lib = load()
-    fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
-    return _Prepared(fn, args, keep, result)
+    return _Prepared(_partial_fn(lib, tokens, no_alloc), args, keep, result)
 
 
 def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
                         scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
-                        n_splits=0, row_tile=0, stream=None, tokens=False):
+                        n_splits=0, row_tile=0, stream=None, tokens=False, no_alloc=False):
     """Partial attention of each job's Mq x H rows over its selected blocks,
     or with tokens=True over its selected single tokens (sel_block_ids then
-    holds logical token ids, block * 64 + t).
+    holds logical token ids, block * 64 + t).  no_alloc=True calls the
+    allocation-free entry point (split-K partials in the library's static
+    scratch array; block selections only).
 
     Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
     """
@@ -244,8 +255,7 @@ def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_
     args, _keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                         sel_block_ids, scale, out_lat, out_lse, ckv_scale,
                                         kpe_scale, n_splits, row_tile, stream)
-    fn = lib.mla_sparse_partial_attn_tokens if tokens else lib.mla_sparse_partial_attn_ex
-    _check(lib, fn(*args))
+    _check(lib, _partial_fn(lib, tokens, no_alloc)(*args))
     return result
 
 
