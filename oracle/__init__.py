@@ -38,7 +38,7 @@ def _load(path=None):
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     lib.oracle_partial.restype = i32
     lib.oracle_partial.argtypes = [i32, i32, i32, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp,
-                                   vp, vp, i32, i32, dbl, vp, vp, i32]
+                                   vp, vp, i32, i32, dbl, vp, vp, vp, vp, i32]
     lib.oracle_merge.restype = i32
     lib.oracle_merge.argtypes = [i32, i64, i32, vp, vp, vp, vp, i32]
     lib.oracle_bf16_to_f64.restype = dbl
@@ -70,7 +70,7 @@ def e4m3fn_to_f64(code):
 
 
 def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=None,
-            n_threads=None, lib=None, tokens=False):
+            n_threads=None, lib=None, tokens=False, stats=False):
     """Oracle partial attention.
 
     q_lat uint16 [R, Mq, H, 512] and q_pe uint16 [R, Mq, H, 64] hold bf16 bits;
@@ -80,7 +80,9 @@ def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=
     [R, Mq, K] (one per query row); -1 = empty slot.  A slot names a logical
     block (all 64 tokens), or with tokens=True one logical token s (token
     s % 64 of logical block s // 64).
-    Returns (out float64 [R, Mq, H, 512], lse float64 [R, Mq, H]).
+    Returns (out float64 [R, Mq, H, 512], lse float64 [R, Mq, H]); with
+    stats=True also the largest score M and the denominator l = sum exp(s - M)
+    of every row (float64 [R, Mq, H]; -inf and 0 for an empty row).
     """
     lib = lib or _load()
     q_lat = np.ascontiguousarray(q_lat, dtype=np.uint16)
@@ -107,13 +109,15 @@ def partial(q_lat, q_pe, ckv, kpe, table, sel, scale, ckv_scale=None, kpe_scale=
     assert table.shape[0] == R and sel.shape[0] == R and (not per_row or sel.shape[1] == Mq)
     out = np.zeros((R, Mq, H, DLAT), np.float64)
     lse = np.zeros((R, Mq, H), np.float64)
+    mx = np.zeros((R, Mq, H), np.float64) if stats else None
+    den = np.zeros((R, Mq, H), np.float64) if stats else None
     rc = lib.oracle_partial(R, Mq, H, P, NB, K, _ptr(q_lat), _ptr(q_pe), kind, _ptr(ckv),
                             _ptr(kpe), _ptr(cs), _ptr(ks), _ptr(table), _ptr(sel),
                             int(per_row), int(bool(tokens)), float(scale), _ptr(out), _ptr(lse),
-                            int(n_threads or default_threads()))
+                            _ptr(mx), _ptr(den), int(n_threads or default_threads()))
     if rc != 0:
         raise ValueError("oracle_partial: invalid selected id or table entry")
-    return out, lse
+    return (out, lse, mx, den) if stats else (out, lse)
 
 
 def merge(parts_o, parts_lse, n_threads=None, lib=None):

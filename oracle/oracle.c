@@ -108,6 +108,10 @@ static double kpe_at(const kv_view* kv, int64_t b, int t, int d) {
  *                  1: a slot names one logical token s of the chunk, token
  *                  s % 64 of logical block s / 64
  *   out   [R][Mq][H][512], lse [R][Mq][H]        double, written
+ *   max_out, denom_out [R][Mq][H]                double, written unless NULL:
+ *                  the two softmax statistics of Section 3.2's wire partial,
+ *                  the largest score M and the denominator l = sum_T exp(s - M)
+ *                  (so lse = M + ln l); an empty T gives M = -inf, l = 0
  *
  * For job r and row (i, h), with T the multiset of tokens (b, t) selected
  * for the row (by the job, or by query row i):
@@ -124,7 +128,7 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
                    const void* ckv, const void* kpe, const float* ckv_scale,
                    const float* kpe_scale, const int32_t* table, const int32_t* sel,
                    int sel_per_row, int sel_tokens, double scale, double* out, double* lse,
-                   int n_threads) {
+                   double* max_out, double* denom_out, int n_threads) {
   kv_view kv = {kv_kind, ckv, kpe, ckv_scale, kpe_scale};
   int bad = 0;
   if (kv_kind != ORACLE_KV_BF16 && kv_kind != ORACLE_KV_E4M3FN) return -1;
@@ -165,6 +169,8 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
     for (int d = 0; d < ORACLE_DLAT; ++d) o[d] = 0.0;
     if (n_tok == 0) {
       lse[row] = -INFINITY;
+      if (max_out) max_out[row] = -INFINITY;
+      if (denom_out) denom_out[row] = 0.0;
       continue;
     }
     double* score = (double*)malloc(sizeof(double) * (size_t)n_tok);
@@ -204,6 +210,8 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K,
     for (int k = 0; k < n; ++k) l += exp(score[k] - M);
     double L = M + log(l);
     lse[row] = L;
+    if (max_out) max_out[row] = M;
+    if (denom_out) denom_out[row] = l;
     for (int k = 0; k < n; ++k) {
       double w = exp(score[k] - L);
       for (int d = 0; d < ORACLE_DLAT; ++d) o[d] += w * ckv_at(&kv, blk[k], tok[k], d);

@@ -60,9 +60,11 @@ def _kv_value(w, which, b, t, d):
     return -v if c & 0x80 else v
 
 
-def brute_force(w, rows=None):
+def brute_force(w, rows=None, stats=None):
     """Partial attention by the definition, without the max shift.
-    Returns {(r, i, h): (out list, lse float)} for the requested rows."""
+    Returns {(r, i, h): (out list, lse float)} for the requested rows; a dict
+    given as stats receives {(r, i, h): (M, l)}, the largest score and
+    sum exp(s - M) (Section 3.2's wire statistics), from the same scores."""
     R, Mq, H, _ = w.q_lat.shape
     mpmath.mp.dps = 40
     res = {}
@@ -80,10 +82,13 @@ def brute_force(w, rows=None):
             toks.extend((b, t) for t in range(BLOCK))
         if not toks:
             res[(r, i, h)] = ([0.0] * DLAT, -math.inf)
+            if stats is not None:
+                stats[(r, i, h)] = (-math.inf, 0.0)
             continue
         ql = [_bf16_struct(x) for x in w.q_lat[r, i, h]]
         qp = [_bf16_struct(x) for x in w.q_pe[r, i, h]]
         weights = []
+        scores = []
         for (b, t) in toks:
             key = (b, t)
             if key not in cache_v:
@@ -91,8 +96,12 @@ def brute_force(w, rows=None):
                                 [_kv_value(w, "kpe", b, t, d) for d in range(DPE)])
             kv, kp = cache_v[key]
             dot = math.fsum([a * c for a, c in zip(ql, kv)] + [a * c for a, c in zip(qp, kp)])
-            weights.append(mpmath.exp(mpmath.mpf(w.scale) * mpmath.mpf(dot)))
+            scores.append(mpmath.mpf(w.scale) * mpmath.mpf(dot))
+            weights.append(mpmath.exp(scores[-1]))
         z = mpmath.fsum(weights)
+        if stats is not None:
+            m = max(scores)
+            stats[(r, i, h)] = (float(m), float(mpmath.fsum(mpmath.exp(x - m) for x in scores)))
         lse = float(mpmath.log(z))
         pw = [float(x / z) for x in weights]
         out = [math.fsum(pw[k] * cache_v[toks[k]][0][d] for k in range(len(toks)))
@@ -165,6 +174,30 @@ def pin_bruteforce_negative_scale(lib):
                             scale=-0.3)
     out, lse = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale, lib=lib)
     _check_rows(out, lse, brute_force(w), 1e-12, 1e-12)
+
+
+def pin_bruteforce_wire_stats(lib):
+    """The largest score M and the denominator l of every row (the two
+    statistics Section 3.2 ships with the bf16 partial) against brute force,
+    over block, fp8, per-row and token selections with empty rows."""
+    cases = [W.tiny(),
+             W.random_case(31, R=2, Mq=2, H=3, P=6, NB=4, K=3, n_valid=[0, 2]).to_fp8(False),
+             W.random_case(32, R=1, Mq=3, H=2, P=5, NB=4, K=3, per_row=True,
+                           n_valid=[[3, 0, 1]]),
+             W.random_case(33, R=2, Mq=1, H=3, P=5, NB=3, K=40, tokens=True, n_valid=[40, 7])]
+    for w in cases:
+        st = {}
+        brute_force(w, stats=st)
+        out, lse, mx, den = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                                           w.ckv_scale, w.kpe_scale, lib=lib, tokens=w.tokens,
+                                           stats=True)
+        for (r, i, h), (m_ref, l_ref) in st.items():
+            if m_ref == -math.inf:
+                assert mx[r, i, h] == -math.inf and den[r, i, h] == 0.0, (w.name, r, i, h)
+                continue
+            assert abs(mx[r, i, h] - m_ref) <= 1e-12 * max(1.0, abs(m_ref)), (w.name, r, i, h)
+            assert abs(den[r, i, h] - l_ref) <= 1e-12 * l_ref and den[r, i, h] >= 1.0
+            assert abs(lse[r, i, h] - (m_ref + math.log(l_ref))) <= 1e-12 * max(1.0, abs(m_ref))
 
 
 def pin_per_row_is_one_job_per_row(lib):
@@ -506,4 +539,4 @@ ALL_PINS = [pin_bf16_decode, pin_e4m3_decode, pin_bruteforce_tiny, pin_bruteforc
             pin_bruteforce_fp8, pin_dense_equals_library, pin_identical_tokens,
             pin_identical_keys_mean, pin_zero_query, pin_two_groups, pin_one_hot,
             pin_empty_and_duplicates, pin_merge_partition, pin_merge_algebra,
-            pin_merge_zero_weight, pin_bruteforce_negative_scale]
+            pin_merge_zero_weight, pin_bruteforce_negative_scale, pin_bruteforce_wire_stats]

@@ -58,12 +58,15 @@ MUTANTS = [
     ("query_row_of_job", "const uint16_t* ql = q_lat + row * ORACLE_DLAT;",
      "const uint16_t* ql = q_lat + (int64_t)r * ORACLE_DLAT;"),
     ("job_index_ignores_mq", "int r = (int)(row / ((int64_t)Mq * H));", "int r = (int)(row / H);"),
-    ("empty_lse_zero", "      lse[row] = -INFINITY;\n      continue;",
-     "      lse[row] = 0.0;\n      continue;"),
+    ("empty_lse_zero", "      lse[row] = -INFINITY;\n      if (max_out)",
+     "      lse[row] = 0.0;\n      if (max_out)"),
     ("rope_query_uses_latent",
      "dot += oracle_bf16_to_f64(qp[d]) * kpe_at(&kv, b, t, d);",
      "dot += oracle_bf16_to_f64(ql[d]) * kpe_at(&kv, b, t, d);"),
     ("max_is_min", "if (score[k] > M) M = score[k];", "if (score[k] < M) M = score[k];"),
+    ("wire_max_is_lse", "if (max_out) max_out[row] = M;", "if (max_out) max_out[row] = L;"),
+    ("wire_denom_unshifted", "if (denom_out) denom_out[row] = l;",
+     "if (denom_out) denom_out[row] = l * exp(M);"),
 ]
 
 _RUNNER = r"""

@@ -23,7 +23,8 @@ int oracle_partial(int R, int Mq, int H, int64_t P, int NB, int K, const uint16_
                    const uint16_t* q_pe, int kv_kind, const void* ckv, const void* kpe,
                    const float* ckv_scale, const float* kpe_scale, const int32_t* table,
                    const int32_t* sel, int sel_per_row, int sel_tokens, double scale,
-                   double* out, double* lse, int n_threads);
+                   double* out, double* lse, double* max_out, double* denom_out,
+                   int n_threads);
 int oracle_merge(int n_parts, int64_t n_rows, int dv, const double* o, const double* lam,
                  double* out, double* lse_out, int n_threads);
 
@@ -53,17 +54,19 @@ int main(void) {
   for (int i = 0; i < R * K; ++i) sel_tok[i] = (int32_t)(next() % (NB * 64 + 1)) - 1;
   double* out = malloc(sizeof(double) * R * MQ * H * 512);
   double* lse = malloc(sizeof(double) * R * MQ * H);
+  double* mx = malloc(sizeof(double) * R * MQ * H);
+  double* den = malloc(sizeof(double) * R * MQ * H);
   int rc = 0;
-  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel, 0, 0, 0.07, out, lse, 2);
-  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 1, ckv8, kpe8, cs, ks, table, sel, 0, 0, 0.07, out, lse, 2);
-  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel_rows, 1, 0, 0.07, out, lse, 2);
-  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel_tok, 0, 1, 0.07, out, lse, 2);
-  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 1, ckv8, kpe8, cs, ks, table, sel_tok, 0, 1, 0.07, out, lse, 2);
+  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel, 0, 0, 0.07, out, lse, NULL, NULL, 2);
+  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 1, ckv8, kpe8, cs, ks, table, sel, 0, 0, 0.07, out, lse, mx, den, 2);
+  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel_rows, 1, 0, 0.07, out, lse, mx, den, 2);
+  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, sel_tok, 0, 1, 0.07, out, lse, NULL, NULL, 2);
+  rc |= oracle_partial(R, MQ, H, P, NB, K, ql, qp, 1, ckv8, kpe8, cs, ks, table, sel_tok, 0, 1, 0.07, out, lse, NULL, NULL, 2);
   if (rc != 0) { fprintf(stderr, "valid calls failed\n"); return 2; }
   int32_t bad[R * K];
   memcpy(bad, sel, sizeof bad);
   bad[3] = NB;  /* out of range: the call reports it */
-  if (oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, bad, 0, 0, 0.07, out, lse, 2) != -1) {
+  if (oracle_partial(R, MQ, H, P, NB, K, ql, qp, 0, ckv, kpe, NULL, NULL, table, bad, 0, 0, 0.07, out, lse, NULL, NULL, 2) != -1) {
     fprintf(stderr, "invalid id not reported\n");
     return 3;
   }
@@ -72,7 +75,7 @@ int main(void) {
   for (int i = 0; i < N * ROWS * DV; ++i) o[i] = (double)(next() % 1000) / 500.0 - 1.0;
   for (int i = 0; i < N * ROWS; ++i) lam[i] = (i % 5 == 0) ? -INFINITY : (double)(next() % 100) / 10.0;
   if (oracle_merge(N, ROWS, DV, o, lam, mo, ml, 2) != 0) return 4;
-  free(ql); free(qp); free(ckv); free(kpe); free(ckv8); free(kpe8); free(out); free(lse);
+  free(ql); free(qp); free(ckv); free(kpe); free(ckv8); free(kpe8); free(out); free(lse); free(mx); free(den);
   puts("ok");
   return 0;
 }
