@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define MLA_SPARSE_VERSION 2
+#define MLA_SPARSE_VERSION 3
 
 #define MLA_DLAT 512  /* latent width = d_v (Section 3.2)                    */
 #define MLA_DPE 64    /* decoupled-RoPE width = d_qk - d_v (Section 3.2)      */
@@ -124,6 +124,12 @@ typedef struct {
  *                                     accumulated in fp32)
  *   out_lat           [R, Mq, H, 512] fp32   written: normalised partial output
  *   out_lse           [R, Mq, H]      fp32   written: natural-log log-sum-exp
+ *                 (with opts.out_format = MLA_OUT_BF16_WIRE, the wire form of
+ *                 Section 3.2, 1032 bytes per row: out_lat [R, Mq, H, 512]
+ *                 bf16, the normalised output rounded to nearest even, and
+ *                 out_lse [R, Mq, H, 2] fp32 holding (m, l): the largest score
+ *                 m of the row's tokens and l = sum_T exp(s_t - m), so that
+ *                 out_lse = m + ln l; an empty T gives (-inf, 0))
  *
  * For each row, with T the multiset of tokens of the blocks selected for it
  * (by its job, or by its query row),
@@ -172,8 +178,13 @@ typedef struct {
   /* rows per work item: 64 or 128 (0 = automatic: 128 when Mq * H > 64 and
    * the splits are long, else 64). */
   int32_t row_tile;
-  int32_t reserved[6]; /* must be zero */
+  /* output form: MLA_OUT_FP32 (0) or MLA_OUT_BF16_WIRE (see the partial
+   * call's out_lat / out_lse). */
+  int32_t out_format;
+  int32_t reserved[5]; /* must be zero */
 } mla_partial_opts_t;
+
+enum { MLA_OUT_FP32 = 0, MLA_OUT_BF16_WIRE = 1 };
 
 /* mla_sparse_partial_attn with explicit options (opts may be NULL). */
 mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
@@ -256,6 +267,10 @@ mla_status_t mla_sparse_partial_attn_tokens(const mla_tensor_t* q_lat, const mla
  * A part whose lse is -inf is skipped whatever its out_lat holds (even NaN);
  * if no part is live the row is 0.  The parts may live anywhere but must
  * share one set of strides; out may not overlap any input.
+ * Parts in the bf16 wire form (Section 3.2; see mla_partial_opts_t
+ * out_format) are accepted too: out_lat[j] [B, Mq, H, 512] bf16 with
+ * out_lse[j] [B, Mq, H, 2] fp32 pairs (m, l), whose lse is m + ln l (-inf
+ * when l = 0); every part must then be in that form.  out stays fp32.
  */
 mla_status_t mla_merge_partials(const mla_tensor_t* const* out_lat,
                                 const mla_tensor_t* const* out_lse, int32_t n_parts,

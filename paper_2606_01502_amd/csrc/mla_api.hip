@@ -228,11 +228,15 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     const char* sel_name = tokens ? "sel_token_ids" : "sel_block_ids";
     if ((st = check_tensor(sel_block_ids, sel_name, MLA_DTYPE_INT32, per_row ? 3 : 2)) != MLA_OK)
       return st;
-    if ((st = check_tensor(out_lat, "out_lat", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
-    if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
+    const bool wire = opts && opts->out_format == MLA_OUT_BF16_WIRE;
+    if ((st = check_tensor(out_lat, "out_lat", wire ? MLA_DTYPE_BF16 : MLA_DTYPE_FP32, 4)) != MLA_OK)
+      return st;
+    if ((st = check_tensor(out_lse, "out_lse", MLA_DTYPE_FP32, wire ? 4 : 3)) != MLA_OK) return st;
     if (opts) {
-      for (int i = 0; i < 6; ++i)
+      for (int i = 0; i < 5; ++i)
         if (opts->reserved[i]) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.reserved must be zero");
+      if (opts->out_format != MLA_OUT_FP32 && opts->out_format != MLA_OUT_BF16_WIRE)
+        return fail(MLA_ERR_INVALID_ARGUMENT, "opts.out_format must be MLA_OUT_FP32 or MLA_OUT_BF16_WIRE");
       if (opts->n_splits < 0) return fail(MLA_ERR_INVALID_ARGUMENT, "opts.n_splits must be >= 0");
       if (opts->row_tile != 0 && opts->row_tile != 64 && opts->row_tile != 128)
         return fail(MLA_ERR_INVALID_ARGUMENT, "opts.row_tile must be 0, 64 or 128");
@@ -255,7 +259,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     if (sel_block_ids->shape[0] != R || (per_row && sel_block_ids->shape[1] != Mq))
       return fail(MLA_ERR_INVALID_ARGUMENT, "sel_block_ids: shape must be [R, K] or [R, Mq, K]");
     if (!shape_is(out_lat, {R, Mq, H, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat: shape must be [R, Mq, H, 512]");
-    if (!shape_is(out_lse, {R, Mq, H})) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
+    if (!wire && !shape_is(out_lse, {R, Mq, H}))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: shape must be [R, Mq, H]");
+    if (wire && (!shape_is(out_lse, {R, Mq, H, 2}) || out_lse->stride[3] != 1))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse: the wire form takes [R, Mq, H, 2] (m, l) pairs");
     if (ckv_pool->stride[0] != MLA_BLOCK * MLA_DLAT || ckv_pool->stride[1] != MLA_DLAT ||
         kpe_pool->stride[0] != MLA_BLOCK * MLA_DPE || kpe_pool->stride[1] != MLA_DPE)
       return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be contiguous");
@@ -263,7 +270,11 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       return fail(MLA_ERR_INVALID_ARGUMENT, "pools must be 16-byte aligned");
     if (!rows_aligned(*q_lat, 2) || !rows_aligned(*q_pe, 2))
       return fail(MLA_ERR_INVALID_ARGUMENT, "q_lat/q_pe rows must be 16-byte aligned");
-    if (!rows_aligned(*out_lat, 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat rows must be 16-byte aligned");
+    if (!rows_aligned(*out_lat, wire ? 2 : 4))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat rows must be 16-byte aligned");
+    if (wire && ((reinterpret_cast<uintptr_t>(out_lse->data) & 7u) != 0 || out_lse->stride[0] % 2 ||
+                 out_lse->stride[1] % 2 || out_lse->stride[2] % 2))
+      return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse (m, l) pairs must be 8-byte aligned");
     // |scale| <= 2^64 keeps scale * log2(e) and the scores of any bf16 or fp8
     // rows whose dot products stay below 2^63 finite in fp32
     if (!(std::fabs(scale) <= 18446744073709551616.0f))
@@ -397,6 +408,8 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     p.split_by_id = by_id ? 1 : 0;
     p.row_tiles = (int32_t)row_tiles;
     p.scale_log2 = (float)((double)scale * 1.4426950408889634074);
+    p.out_wire = wire ? 1 : 0;
+    p.out16 = (uint16_t*)out_lat->data;
     p.out = (float*)out_lat->data;
     p.out_s0 = out_lat->stride[0]; p.out_s1 = out_lat->stride[1]; p.out_s2 = out_lat->stride[2];
     p.lse = (float*)out_lse->data;
@@ -410,7 +423,7 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       const size_t n_part_rows = (size_t)R * S * rows;
       p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
       const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
-      const size_t ws_bytes = o_bytes + 2 * n_part_rows * sizeof(float);
+      const size_t ws_bytes = o_bytes + 3 * n_part_rows * sizeof(float);
       void* ws = nullptr;
       if (no_alloc) {
         if (ws_bytes > (size_t)MLA_NOALLOC_SCRATCH_BYTES)
@@ -427,6 +440,7 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       p.ws_o16 = (uint16_t*)ws;
       p.ws_scale = (float*)((char*)ws + o_bytes);
       p.ws_lse = p.ws_scale + n_part_rows;
+      p.ws_max = p.ws_lse + n_part_rows;
     }
     const int kv = !fp8 ? mla::kKvBf16
                  : (ckv_pool->block_scale == kpe_pool->block_scale ? mla::kKvFp8Shared
@@ -441,7 +455,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       c.ws_o16 = p.ws_o16;
       c.ws_scale = p.ws_scale;
       c.ws_lse = p.ws_lse;
+      c.ws_max = p.ws_max;
       c.R = (int32_t)R; c.S = (int32_t)S; c.Mq = (int32_t)Mq; c.H = (int32_t)H; c.rows = (int32_t)rows;
+      c.out_wire = p.out_wire;
+      c.out16 = p.out16;
       c.out = p.out; c.out_s0 = p.out_s0; c.out_s1 = p.out_s1; c.out_s2 = p.out_s2;
       c.lse = p.lse; c.lse_s0 = p.lse_s0; c.lse_s1 = p.lse_s1; c.lse_s2 = p.lse_s2;
       e = mla::launch_combine(c, hs);
@@ -664,6 +681,8 @@ mla_status_t mla_merge_partials_ex(const mla_tensor_t* const* out_lat,
     mla_status_t st;
     if ((st = check_tensor(out, "out", MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
     if (out->shape[3] != MLA_DLAT) return fail(MLA_ERR_INVALID_ARGUMENT, "out: last dim must be 512");
+    // parts in the bf16 wire form: bf16 rows with (m, l) pairs
+    const bool wire = out_lat[0] && out_lat[0]->dtype == MLA_DTYPE_BF16;
     if (!rows_aligned(*out, 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "out rows must be 16-byte aligned");
     if (merged_lse) {
       if ((st = check_tensor(merged_lse, "merged_lse", MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
@@ -675,19 +694,26 @@ mla_status_t mla_merge_partials_ex(const mla_tensor_t* const* out_lat,
     std::string nm;
     for (int j = 0; j < n_parts; ++j) {
       nm = "out_lat[" + std::to_string(j) + "]";
-      if ((st = check_tensor(out_lat[j], nm.c_str(), MLA_DTYPE_FP32, 4)) != MLA_OK) return st;
+      if ((st = check_tensor(out_lat[j], nm.c_str(), wire ? MLA_DTYPE_BF16 : MLA_DTYPE_FP32, 4)) != MLA_OK)
+        return st;
       nm = "out_lse[" + std::to_string(j) + "]";
-      if ((st = check_tensor(out_lse[j], nm.c_str(), MLA_DTYPE_FP32, 3)) != MLA_OK) return st;
+      if ((st = check_tensor(out_lse[j], nm.c_str(), MLA_DTYPE_FP32, wire ? 4 : 3)) != MLA_OK) return st;
       for (int d = 0; d < 4; ++d)
         if (out_lat[j]->shape[d] != out->shape[d])
           return fail(MLA_ERR_INVALID_ARGUMENT, "out_lat parts must have the shape of out");
       for (int d = 0; d < 3; ++d)
         if (out_lse[j]->shape[d] != out->shape[d])
           return fail(MLA_ERR_INVALID_ARGUMENT, "out_lse parts must be [B, Mq, H]");
+      if (wire && (out_lse[j]->shape[3] != 2 || out_lse[j]->stride[3] != 1 ||
+                   (reinterpret_cast<uintptr_t>(out_lse[j]->data) & 7u) != 0 ||
+                   out_lse[j]->stride[0] % 2 || out_lse[j]->stride[1] % 2 || out_lse[j]->stride[2] % 2))
+        return fail(MLA_ERR_INVALID_ARGUMENT,
+                    "wire-form parts: out_lse must be [B, Mq, H, 2] fp32 (m, l) pairs, 8-byte aligned");
       for (int d = 0; d < 3; ++d)
         if (out_lat[j]->stride[d] != out_lat[0]->stride[d] || out_lse[j]->stride[d] != out_lse[0]->stride[d])
           return fail(MLA_ERR_UNSUPPORTED, "parts must share one set of strides");
-      if (!rows_aligned(*out_lat[j], 4)) return fail(MLA_ERR_INVALID_ARGUMENT, "part rows must be 16-byte aligned");
+      if (!rows_aligned(*out_lat[j], wire ? 2 : 4))
+        return fail(MLA_ERR_INVALID_ARGUMENT, "part rows must be 16-byte aligned");
       const Extent eo = extent(*out);
       if (overlaps(eo, extent(*out_lat[j])) || overlaps(eo, extent(*out_lse[j])))
         return fail(MLA_ERR_INVALID_ARGUMENT, "out overlaps an input part");
@@ -696,12 +722,13 @@ mla_status_t mla_merge_partials_ex(const mla_tensor_t* const* out_lat,
         if (overlaps(el, extent(*out_lat[j])) || overlaps(el, extent(*out_lse[j])) || overlaps(el, eo))
           return fail(MLA_ERR_INVALID_ARGUMENT, "merged_lse overlaps another tensor");
       }
-      p.o[j] = (const float*)out_lat[j]->data;
+      p.o[j] = out_lat[j]->data;
       p.lse[j] = (const float*)out_lse[j]->data;
     }
     const int64_t B = out->shape[0], Mq = out->shape[1], H = out->shape[2];
     if (B * Mq * H > INT32_MAX / 2) return fail(MLA_ERR_UNSUPPORTED, "too many rows");
     p.n_parts = n_parts;
+    p.wire = wire ? 1 : 0;
     p.B = (int32_t)B; p.Mq = (int32_t)Mq; p.H = (int32_t)H;
     p.o_s0 = out_lat[0]->stride[0]; p.o_s1 = out_lat[0]->stride[1]; p.o_s2 = out_lat[0]->stride[2];
     p.l_s0 = out_lse[0]->stride[0]; p.l_s1 = out_lse[0]->stride[1]; p.l_s2 = out_lse[0]->stride[2];

@@ -39,8 +39,13 @@ struct PartialParams {
   // s takes blocks s, s + n_splits, ... from all K slots of every row
   int32_t split_by_id;
   float scale_log2;  // softmax scale * log2(e)
-  // destination: direct (n_splits == 1) or split-K workspace
+  // destination: direct (n_splits == 1) or split-K workspace.  out_wire: the
+  // bf16 wire form (Section 3.2): bf16 rows at out16 (element strides out_s*)
+  // and (m, l) pairs at lse (pair strides lse_s*, in floats); else fp32 rows
+  // at out and the lse at lse.
+  int32_t out_wire;
   float* out;
+  uint16_t* out16;
   int64_t out_s0, out_s1, out_s2;
   float* lse;
   int64_t lse_s0, lse_s1, lse_s2;
@@ -52,6 +57,7 @@ struct PartialParams {
   uint16_t* ws_o16;  // [R][S][rows][512] fp16 bits
   float* ws_scale;   // [R][S][rows]
   float* ws_lse;     // [R][S][rows]
+  float* ws_max;     // [R][S][rows], the split's largest score (log2 units; wire form)
 };
 
 // Combine of the S split partials of every job into the caller's outputs.
@@ -61,17 +67,23 @@ struct CombineParams {
   const uint16_t* ws_o16;
   const float* ws_scale;
   const float* ws_lse;
+  const float* ws_max;  // the splits' largest scores (log2 units), wire form only
   int32_t R, S, Mq, H, rows;
+  int32_t out_wire;     // see PartialParams
   float* out;
+  uint16_t* out16;
   int64_t out_s0, out_s1, out_s2;
   float* lse;
   int64_t lse_s0, lse_s1, lse_s2;
 };
 
-// Merge of n parts given by pointers with shared strides.
+// Merge of n parts given by pointers with shared strides.  wire: the parts
+// are in the bf16 wire form (bf16 rows, (m, l) pairs at lse[j] with strides
+// l_s* in floats); else fp32 rows and lse values.
 struct MergeParams {
-  const float* o[kMaxParts];
+  const void* o[kMaxParts];
   const float* lse[kMaxParts];
+  int32_t wire;
   int32_t n_parts;
   int32_t B, Mq, H;
   int64_t o_s0, o_s1, o_s2;

@@ -74,6 +74,24 @@ struct F32Rows {
 };
 
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x4_t __attribute__((ext_vector_type(4)));
+
+// bf16 -> fp32 is exact: the bf16 bits are the upper half of the fp32 bits.
+__device__ __forceinline__ f32x4_t bf16x4_f32(u16x4_t a) {
+  return f32x4_t{__uint_as_float((uint32_t)a[0] << 16), __uint_as_float((uint32_t)a[1] << 16),
+                 __uint_as_float((uint32_t)a[2] << 16), __uint_as_float((uint32_t)a[3] << 16)};
+}
+
+// Rows of wire-form parts: bf16.
+struct Bf16Rows {
+  template <typename RowAt>
+  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
+                                              f32x4_t& v1) {
+    const uint16_t* r = row_at(j);
+    v0 = bf16x4_f32(*(const u16x4_t*)(r + 4 * lane));
+    v1 = bf16x4_f32(*(const u16x4_t*)(r + 256 + 4 * lane));
+  }
+};
 
 struct F16Rows {
   template <typename RowAt>
@@ -89,18 +107,20 @@ struct F16Rows {
 
 // Merge n parts of one row.  lse_at(j): part j's lse; row_at(j): part j's
 // row (Rows says how to read it); scale_at(j): the factor part j's stored
-// values carry (1 for fp32 parts).  Writes the 512 outputs at out and
-// returns the merged lse.
+// values carry (1 for fp32 parts).  Leaves the lane's outputs (columns
+// 4 lane .. +3 and 256 + 4 lane .. +3) in acc0, acc1 and returns the merged
+// lse.
 template <typename Rows, typename LseAt, typename RowAt, typename ScaleAt>
 __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, ScaleAt scale_at,
-                                           float* out, int lane) {
+                                           f32x4_t& acc0, f32x4_t& acc1, int lane) {
   float m = -INFINITY;
   for (int j0 = 0; j0 < n; j0 += 64) {
     const int j = j0 + lane;
     if (j < n) m = fmaxf(m, lse_at(j));
   }
   m = wave_max(m);
-  f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  acc0 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  acc1 = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float lse = -INFINITY;
   if (m != -INFINITY) {
     float s = 0.f;
@@ -141,9 +161,23 @@ __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, Sc
       }
     }
   }
+  return lse;
+}
+
+// Stores of a merged row: fp32, or bf16 rounded to nearest even.
+__device__ __forceinline__ void store_row(float* out, f32x4_t acc0, f32x4_t acc1, int lane) {
   *(f32x4_t*)(out + 4 * lane) = acc0;
   *(f32x4_t*)(out + 256 + 4 * lane) = acc1;
-  return lse;
+}
+
+__device__ __forceinline__ u16x4_t f32x4_bf16(f32x4_t v) {
+  return u16x4_t{__builtin_bit_cast(uint16_t, (__bf16)v[0]), __builtin_bit_cast(uint16_t, (__bf16)v[1]),
+                 __builtin_bit_cast(uint16_t, (__bf16)v[2]), __builtin_bit_cast(uint16_t, (__bf16)v[3])};
+}
+
+__device__ __forceinline__ void store_row(uint16_t* out, f32x4_t acc0, f32x4_t acc1, int lane) {
+  *(u16x4_t*)(out + 4 * lane) = f32x4_bf16(acc0);
+  *(u16x4_t*)(out + 256 + 4 * lane) = f32x4_bf16(acc1);
 }
 
 __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
@@ -156,9 +190,24 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
   const int i = rem / p.H, h = rem - (rem / p.H) * p.H;
   const int64_t lo = b * p.l_s0 + i * p.l_s1 + h * p.l_s2;
   const int64_t oo = b * p.o_s0 + i * p.o_s1 + h * p.o_s2;
-  const float lse = merge_row<F32Rows>(
-      p.n_parts, [&](int j) { return p.lse[j][lo]; }, [&](int j) { return p.o[j] + oo; },
-      [](int) { return 1.f; }, p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2, lane);
+  f32x4_t acc0, acc1;
+  float lse;
+  if (p.wire) {
+    // wire-form parts: lse = m + ln l from the (m, l) pair (-inf when l = 0)
+    lse = merge_row<Bf16Rows>(
+        p.n_parts,
+        [&](int j) {
+          const float m = p.lse[j][lo], l = p.lse[j][lo + 1];
+          return l > 0.f ? m + __logf(l) : -INFINITY;
+        },
+        [&](int j) { return (const uint16_t*)p.o[j] + oo; }, [](int) { return 1.f; }, acc0, acc1,
+        lane);
+  } else {
+    lse = merge_row<F32Rows>(
+        p.n_parts, [&](int j) { return p.lse[j][lo]; },
+        [&](int j) { return (const float*)p.o[j] + oo; }, [](int) { return 1.f; }, acc0, acc1, lane);
+  }
+  store_row(p.out + b * p.out_s0 + i * p.out_s1 + h * p.out_s2, acc0, acc1, lane);
   if (p.out_lse && lane == 0) p.out_lse[b * p.ol_s0 + i * p.ol_s1 + h * p.ol_s2] = lse;
 }
 
@@ -176,16 +225,36 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineParams p
   const int row = grow - r * p.rows;
   const int64_t base = (int64_t)r * p.S * p.rows + row;  // split j of (r, row) at base + j*rows
   const int i = row / p.H, h = row - (row / p.H) * p.H;
-  float* out = p.out + r * p.out_s0 + i * p.out_s1 + h * p.out_s2;
+  const int64_t oo = r * p.out_s0 + i * p.out_s1 + h * p.out_s2;
   auto lse_at = [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; };
+  f32x4_t acc0, acc1;
   const float lse =
       p.ws_f16 ? merge_row<F16Rows>(
                      p.S, lse_at, [&](int j) { return p.ws_o16 + (base + (int64_t)j * p.rows) * kDLat; },
-                     [&](int j) { return p.ws_scale[base + (int64_t)j * p.rows]; }, out, lane)
+                     [&](int j) { return p.ws_scale[base + (int64_t)j * p.rows]; }, acc0, acc1, lane)
                : merge_row<F32Rows>(
                      p.S, lse_at, [&](int j) { return p.ws_o32 + (base + (int64_t)j * p.rows) * kDLat; },
-                     [](int) { return 1.f; }, out, lane);
-  if (lane == 0) p.lse[r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2] = lse;
+                     [](int) { return 1.f; }, acc0, acc1, lane);
+  const int64_t lo = r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2;
+  if (!p.out_wire) {
+    store_row(p.out + oo, acc0, acc1, lane);
+    if (lane == 0) p.lse[lo] = lse;
+    return;
+  }
+  // wire form: bf16 row, and (m, l) with m the largest score over the splits
+  // (their maxima, log2 units) and l = exp(lse - m)
+  store_row(p.out16 + oo, acc0, acc1, lane);
+  float m2 = -INFINITY;
+  for (int j0 = 0; j0 < p.S; j0 += 64) {
+    const int j = j0 + lane;
+    if (j < p.S) m2 = fmaxf(m2, p.ws_max[base + (int64_t)j * p.rows]);
+  }
+  m2 = wave_max(m2);
+  if (lane == 0) {
+    const float m = m2 * 0.69314718055994530942f;
+    p.lse[lo] = lse == -INFINITY ? -INFINITY : m;
+    p.lse[lo + 1] = lse == -INFINITY ? 0.f : __expf(lse - m);
+  }
 }
 
 }  // namespace

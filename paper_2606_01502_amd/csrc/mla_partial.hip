@@ -66,6 +66,7 @@ typedef short i16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x4_t __attribute__((ext_vector_type(4)));
 
 #define LDS __attribute__((address_space(3)))
 #define GLOBAL __attribute__((address_space(1)))
@@ -264,6 +265,39 @@ __device__ __forceinline__ void st_pair(f32x4_t& c0, f32x4_t& c1, bf16x8_t a0, b
 }
 #undef MLA_P2
 
+// One S^T product, c += a . q (kFirst: c = a . q), as an asm statement of its
+// own.  A wave issues in order and waits at a product until the matrix core
+// takes it, so only what is placed between single products (key reads,
+// loads of the next block) issues while the matrix core works; after a
+// group of products it would overlap the group's last one only.  kPad ends
+// with the 24 wait states after which VALU code may read c.
+template <bool kFirst, bool kPad, bool kPre = false>
+__device__ __forceinline__ void st1(f32x4_t& c, bf16x8_t a, bf16x8_t q) {
+  // kPre: 3 wait states first, for operands just written by VALU code
+  if constexpr (kFirst && kPre)
+    asm volatile("s_nop 2\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "v"(q));
+  else if constexpr (kFirst)
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "v"(q));
+  else if constexpr (kPad && kPre)
+    asm volatile("s_nop 2\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+v"(c) : "v"(a), "v"(q));
+  else if constexpr (kPad)
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+v"(c) : "v"(a), "v"(q));
+  else if constexpr (kPre)
+    asm volatile("s_nop 2\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(q));
+  else
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(q));
+}
+
+// Ties the computation of x to this point of the instruction stream (an empty
+// volatile asm that reads and writes x), so that the compiler cannot sink it
+// down to its first use, next to the product that reads it.
+template <typename T>
+__device__ __forceinline__ void pin(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
 // x * s for an accumulator tile that lives in the accumulation registers.
 // The empty asm statements keep the tile there: without them the register
 // allocator moves part of O into architectural VGPRs for the whole kernel to
@@ -293,6 +327,12 @@ __device__ __forceinline__ void scale_inplace4(f32x4_t& x, f32x4_t s) {
                : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3)
                : "v"(s[0]), "v"(s[1]), "v"(s[2]), "v"(s[3]));
   x = f32x4_t{x0, x1, x2, x3};
+}
+
+// Four floats -> four bf16 (round to nearest even).
+__device__ __forceinline__ u16x4_t f32x4_bf16(f32x4_t v) {
+  return u16x4_t{__builtin_bit_cast(uint16_t, (__bf16)v[0]), __builtin_bit_cast(uint16_t, (__bf16)v[1]),
+                 __builtin_bit_cast(uint16_t, (__bf16)v[2]), __builtin_bit_cast(uint16_t, (__bf16)v[3])};
 }
 
 // Two floats -> two fp16 (round to nearest even), packed low first.
@@ -611,10 +651,11 @@ __device__ __forceinline__ void put_fp8_factors(LDS float* scales, int i, float 
 
 // Compact the valid selected blocks of slots [slot0, slot0 + nslots) of job r
 // into the LDS list (slot order kept); for fp8 also each listed block's
-// factors (put_fp8_factors).  Returns the number of listed blocks.
+// factors (put_fp8_factors).  first_id: the id of slot slot0 + tid, already
+// loaded (see first_slot_id).  Returns the number of listed blocks.
 template <bool FP8>
 __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int slot0, int nslots,
-                                             LDS uint8_t* smem, int tid) {
+                                             int first_id, LDS uint8_t* smem, int tid) {
   using L = Layout<FP8>;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -626,7 +667,7 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
     const int i = base + tid;
     int b = -1;
     if (i < nslots) {
-      const int id = p.sel[r * p.sel_s0 + slot0 + i];
+      const int id = base == 0 ? first_id : p.sel[r * p.sel_s0 + slot0 + i];
       if (id >= 0 && id < p.NB) {
         const int bb = p.table[r * p.table_s0 + id];
         if (bb >= 0 && bb < p.P) b = bb;
@@ -664,10 +705,12 @@ __device__ __forceinline__ int compact_slots(const PartialParams& p, int r, int 
 // row) of the blocks taken; at most nslots each) use the stage area, which is
 // free until the first load is issued.  Returns the number of entries.
 // fp8: each entry also gets its block's factors (put_fp8_factors).
+// first_id: the id of this thread's first entry (row i0 + tid / nslots, slot
+// slot0 + tid % nslots), already loaded.
 template <bool FP8>
 __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, int slot0,
                                                int nslots, int id0, int id_step, int i0, int n_i,
-                                               LDS uint8_t* smem, LDS int* list,
+                                               int first_id, LDS uint8_t* smem, LDS int* list,
                                                LDS uint64_t* masks, int tid) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -682,7 +725,7 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
   const int n_ent = n_i * nslots;
   for (int e = tid; e < n_ent; e += 256) {
     const int ii = e / nslots, j = e - ii * nslots;
-    const int id = p.sel[r * p.sel_s0 + (int64_t)(i0 + ii) * p.sel_s1 + slot0 + j];
+    const int id = e == tid ? first_id : p.sel[r * p.sel_s0 + (int64_t)(i0 + ii) * p.sel_s1 + slot0 + j];
     const int u = (id - id0) / id_step;
     if (id >= id0 && id < p.NB && u * id_step == id - id0) {
       const int bb = p.table[r * p.table_s0 + id];
@@ -741,14 +784,16 @@ __device__ __forceinline__ int compact_per_row(const PartialParams& p, int r, in
 // nslots) of job r into the LDS list as pool tokens (table[r, id / 64] * 64 +
 // id % 64), slot order kept, and fill the list up to the next multiple of 64
 // with the first entry, so that the last virtual block loads only listed
-// tokens (the fill is masked out of the softmax).  fp8: each token carries
+// tokens (the fill is masked out of the softmax).  first_id as for
+// compact_slots.  fp8: each token carries
 // its own block's factors (fp8_factors): the value scale in tok_scales[i],
 // the RoPE ratio in tok_scales[kMaxSlotsPerSplit + i] and the score factor
 // in tok_scales[2 kMaxSlotsPerSplit + i].  Returns the number of listed
 // tokens.
 template <bool FP8>
 __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int slot0,
-                                              int nslots, LDS uint8_t* smem, int tid) {
+                                              int nslots, int first_id, LDS uint8_t* smem,
+                                              int tid) {
   using L = Layout<FP8>;
   LDS float* tok_scales = (LDS float*)(smem + L::kScales);
   const int lane = tid & 63;
@@ -761,7 +806,7 @@ __device__ __forceinline__ int compact_tokens(const PartialParams& p, int r, int
     const int i = base + tid;
     int pt = -1;
     if (i < nslots) {
-      const int id = p.sel[r * p.sel_s0 + slot0 + i];
+      const int id = base == 0 ? first_id : p.sel[r * p.sel_s0 + slot0 + i];
       if (id >= 0 && id < n_ids) {
         const int bb = p.table[r * p.table_s0 + (id >> 6)];
         if (bb >= 0 && bb < p.P) pt = bb * kBlock + (id & (kBlock - 1));
@@ -845,31 +890,70 @@ void partial_kernel(const PartialParams p) {
   const int slot0 = s_idx * p.slots_per_split;
   const int nslots = max(0, min(p.K - slot0, p.slots_per_split));
 
-  // ---- compact the valid selected blocks of the slot range (slot order kept;
-  // per-row selections: the union over the tile's query rows, with row masks)
+  // ---- prologue.  Three dependent trips to memory (slot ids, block table,
+  // then the first blocks) come before the first product; the query rows go
+  // out between the first two, so that their latency hides behind the
+  // compaction's.
   LDS int* list = (LDS int*)(smem + L::kList);
   LDS float* scales = (LDS float*)(smem + L::kScales);
   LDS uint64_t* masks = (LDS uint64_t*)(smem + L::kMasks);
   const int i0 = rt * kRowsWg / p.H;  // first query row of the tile
+  // per-row selections: the query rows of the tile; split by logical block
+  // (split s takes blocks s, s + S, ... from every slot), so that rows which
+  // chose one block in different slots share its load, or by slot range when
+  // a tile's slots may not fit one list
+  const int n_i = PR ? (min((rt + 1) * kRowsWg, p.rows) - 1) / p.H - i0 + 1 : 1;
+  const int c_slot0 = PR && p.split_by_id ? 0 : slot0;
+  const int c_nslots = PR && p.split_by_id ? p.K : nslots;
+  // the slot id this thread compacts first
+  int first_id = -1;
+  if constexpr (PR) {
+    if (tid < n_i * c_nslots) {
+      const int ii = tid / c_nslots, j = tid - ii * c_nslots;
+      first_id = p.sel[r * p.sel_s0 + (int64_t)(i0 + ii) * p.sel_s1 + c_slot0 + j];
+    }
+  } else {
+    if (tid < nslots) first_id = p.sel[r * p.sel_s0 + slot0 + tid];
+  }
+
+  // this wave's query rows as MFMA B operands, held for the whole kernel:
+  // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
+  // dims 32ks' + 8g .. +7 (ks' = the step within its part).
+  const int row_wg0 = rt * kRowsWg;
+  bf16x8_t qb[RG][18];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
+    if (row < p.rows) {
+      const int i = row / p.H, h = row - (row / p.H) * p.H;
+      const uint16_t* ql = p.q_lat + r * p.ql_s0 + i * p.ql_s1 + h * p.ql_s2 + g * 8;
+      const uint16_t* qp = p.q_pe + r * p.qp_s0 + i * p.qp_s1 + h * p.qp_s2 + g * 8;
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks) qb[rg][ks] = *(const bf16x8_t*)(ql + ks * 32);
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) qb[rg][16 + ks] = *(const bf16x8_t*)(qp + ks * 32);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 18; ++ks) qb[rg][ks] = bf16x8_t{};
+    }
+  }
+
+  // compact the valid selected blocks of the slot range (slot order kept;
+  // per-row selections: the union over the tile's query rows, with row masks)
   int n_valid;
   int n_tok = 0;  // token selections: the listed tokens (n_valid counts virtual blocks)
   if constexpr (PR) {
-    const int n_i = (min((rt + 1) * kRowsWg, p.rows) - 1) / p.H - i0 + 1;
-    // split by logical block (split s takes blocks s, s + S, ... from every
-    // slot), so that rows which chose one block in different slots share its
-    // load; or by slot range when a tile's slots may not fit one list
-    n_valid = p.split_by_id
-                  ? compact_per_row<FP8>(p, r, 0, p.K, s_idx, p.n_splits, i0, n_i, smem, list, masks, tid)
-                  : compact_per_row<FP8>(p, r, slot0, nslots, 0, 1, i0, n_i, smem, list, masks, tid);
+    n_valid = compact_per_row<FP8>(p, r, c_slot0, c_nslots, p.split_by_id ? s_idx : 0,
+                                   p.split_by_id ? p.n_splits : 1, i0, n_i, first_id, smem, list,
+                                   masks, tid);
   } else if constexpr (TOK) {
-    n_tok = compact_tokens<FP8>(p, r, slot0, nslots, smem, tid);
+    n_tok = compact_tokens<FP8>(p, r, slot0, nslots, first_id, smem, tid);
     n_valid = (n_tok + kBlock - 1) / kBlock;
   } else {
-    n_valid = compact_slots<FP8>(p, r, slot0, nslots, smem, tid);
+    n_valid = compact_slots<FP8>(p, r, slot0, nslots, first_id, smem, tid);
   }
 
-  // ---- the first blocks' loads go out before the query rows, so that their
-  // latencies overlap
+  // the first blocks' loads
   if constexpr (TOK && FP8) {
     for (int h = 0; h < n_valid && h < L::kLead; ++h) {
       TokIssue8 ti;
@@ -892,28 +976,6 @@ void partial_kernel(const PartialParams p) {
     for (int h = 0; h < n_valid && h < L::kLead; ++h)
       issue_stage<FP8>(p, list[h], stage0 + h * L::kStage, wave, lane);
   }
-
-  // ---- this wave's query rows as MFMA B operands, held for the whole kernel:
-  // k-step ks (0..15 latent, 16..17 RoPE) covers 32 dims, lane group g takes
-  // dims 32ks' + 8g .. +7 (ks' = the step within its part).
-  const int row_wg0 = rt * kRowsWg;
-  bf16x8_t qb[RG][18];
-#pragma unroll
-  for (int rg = 0; rg < RG; ++rg) {
-    const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
-    if (row < p.rows) {
-      const int i = row / p.H, h = row - (row / p.H) * p.H;
-      const uint16_t* ql = p.q_lat + r * p.ql_s0 + i * p.ql_s1 + h * p.ql_s2 + g * 8;
-      const uint16_t* qp = p.q_pe + r * p.qp_s0 + i * p.qp_s1 + h * p.qp_s2 + g * 8;
-#pragma unroll
-      for (int ks = 0; ks < 16; ++ks) qb[rg][ks] = *(const bf16x8_t*)(ql + ks * 32);
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) qb[rg][16 + ks] = *(const bf16x8_t*)(qp + ks * 32);
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < 18; ++ks) qb[rg][ks] = bf16x8_t{};
-    }
-  }
   // Q (and with it the first stages) is resident before the main loop, so
   // that the only vector-memory operations in flight inside the loop are the
   // prefetches the loop issues itself.
@@ -925,6 +987,8 @@ void partial_kernel(const PartialParams p) {
 #pragma unroll
     for (int rg = 0; rg < RG; ++rg) O[dt][rg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run[RG], l_run[RG];
+  // the largest score of each row so far (log2 units): the wire form's m
+  float m_true[RG];
   // per-row selections: the bit of each of the lane's rows in the entry masks
   // (rows past the end of the job are never stored; any bit will do)
   int row_bit[RG];
@@ -937,6 +1001,7 @@ void partial_kernel(const PartialParams p) {
   for (int rg = 0; rg < RG; ++rg) {
     m_run[rg] = -INFINITY;
     l_run[rg] = 0.f;
+    m_true[rg] = -INFINITY;
   }
 
   // ---- main loop over the listed blocks; L::kLead blocks stream in while one
@@ -972,7 +1037,7 @@ void partial_kernel(const PartialParams p) {
     // steps, beside the products, with the per-block address parts computed
     // once (all 18 at once would hold the four waves for about 1.6k cycles at
     // the per-CU address unit, which takes one 1 KiB load per ~16 cycles).
-    // fp8 (9 loads): all at once after the first key reads.
+    // fp8 (9 loads): one per two S^T steps.
     LDS uint8_t* const next_buf = stage0 + (hn % L::kNum) * L::kStage;
     typename std::conditional<TOK, TokIssue, Bf16Issue>::type bi;
     if constexpr (TOK && !FP8) {
@@ -986,20 +1051,6 @@ void partial_kernel(const PartialParams p) {
       bi.m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + (uint32_t)wave * 16384u);
       bi.lds_rope = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)next_buf + 65536u + (uint32_t)wave * 2048u);
     }
-    auto issue_next = [&]() {
-      if constexpr (TOK) {
-        if (b_next >= 0) {
-          TokIssue8 ti;
-          ti.tok = list[hn * kBlock + 16 * wave + (lane & 15)];
-          ti.buf = (uint32_t)(uintptr_t)next_buf;
-#pragma unroll
-          for (int j = 0; j < L::kLoads; ++j) ti.load(p, j, wave, lane);
-        }
-      } else {
-        if (b_next >= 0) issue_stage<FP8>(p, b_next, next_buf, wave, lane);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    };
     // Per-lane LDS offsets are recomputed from an opaque copy of the lane id in
     // every iteration (a few VALU ops) rather than held in registers across
     // the loop.
@@ -1056,6 +1107,15 @@ void partial_kernel(const PartialParams p) {
             a[tau] = lds_b128(cb + tau * 16384 + (key_base ^ (ks << 6)));
         }
       };
+      // bf16: the fragment of one token tile
+      auto key_frag = [&](int step, int tau, bf16x8_t& a) {
+        if constexpr (!FP8) {
+          if (step < 2)
+            a = lds_b128(cb + tau * 2048 + rope_base + (((4 * step + lg) ^ (ln16 >> 1)) << 4));
+          else
+            a = lds_b128(cb + tau * 16384 + (key_base ^ ((step - 2) << 6)));
+        }
+      };
       auto key_ops = [&](const KRing (&r)[kTau4], bf16x8_t (&a)[kTau4]) {
 #pragma unroll
         for (int tau = 0; tau < kTau4; ++tau) {
@@ -1071,19 +1131,20 @@ void partial_kernel(const PartialParams p) {
       bf16x8_t ka[2][kTau4];
       key_frags(0, kr[0]);
       key_frags(1, kr[1]);
-      if constexpr (FP8) issue_next();
       key_ops(kr[0], ka[0]);
 #pragma unroll
       for (int step = 0; step < 18; ++step) {
-        if (step + 2 < 18) key_frags(step + 2, kr[(step + 2) % 3]);
+        if (FP8 && step + 2 < 18) key_frags(step + 2, kr[(step + 2) % 3]);
         if constexpr (FP8) {
-          // Four pairs of products; after pair j the codes of token tile j of
-          // the next step are converted (4 VALU ops beside the matrix core).
-          // Every converted operand is read at least two products later.
+          // Single products, tile by tile; after the products of tile t the
+          // codes of tile t of the next step are converted to bf16 (4 VALU
+          // ops beside the matrix core), 3 RG products before the first one
+          // that reads them; one load of a later block per two steps.
           __builtin_amdgcn_sched_barrier(0);
           const int ks = step < 2 ? 16 + step : step - 2;
           const bf16x8_t(&a)[kTau4] = ka[step % 2];
-          if (kSplitScales && step == 2) {
+          const bool ratio_step = kSplitScales && step == 2;
+          if (ratio_step) {
 #pragma unroll
             for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
@@ -1092,64 +1153,69 @@ void partial_kernel(const PartialParams p) {
                 else scale_inplace(sacc[rg][tau], pe_ratio);
               }
           }
+          constexpr int kPer = RG * kTau4;
 #pragma unroll
-          for (int j = 0; j < 2 * RG; ++j) {
-            const int rg = j >> 1, t0 = 2 * (j & 1);
-            f32x4_t& c0 = sacc[rg][t0];
-            f32x4_t& c1 = sacc[rg][t0 + 1];
+          for (int j = 0; j < kPer; ++j) {
+            const int tau = j / RG, rg = j % RG;
             const bf16x8_t q = qb[rg][ks];
-            const bool last = j == 2 * RG - 1;
+            // the RoPE steps end with the wait states the ratio's VALU reads
+            // of the results need; the last step with those any read needs
+            const bool pad = (step == 17 || (kSplitScales && step == 1)) && j == kPer - 1;
             if (step == 0)
-              st_pair<true, false, true>(c0, c1, a[t0], a[t0 + 1], q);
-            else if ((step == 17 || (kSplitScales && step == 1)) && last)
-              st_pair<false, true, false>(c0, c1, a[t0], a[t0 + 1], q);
-            else if (kSplitScales && step == 2)
-              // every pair leads with the wait states: the ratio's VALU
-              // writes, and any register copies the compiler places after
-              // them, may end right before it
-              st_pair<false, false, true>(c0, c1, a[t0], a[t0 + 1], q);
+              st1<true, false, true>(sacc[rg][tau], a[tau], q);
+            else if (pad)
+              st1<false, true, false>(sacc[rg][tau], a[tau], q);
+            else if (ratio_step)
+              // every product of this step leads with the wait states: the
+              // ratio's VALU writes of the accumulators come right before
+              st1<false, false, true>(sacc[rg][tau], a[tau], q);
             else
-              st_pair<false, false, false>(c0, c1, a[t0], a[t0 + 1], q);
+              st1<false, false, false>(sacc[rg][tau], a[tau], q);
             __builtin_amdgcn_sched_barrier(0);
-            const int tc = j * kTau4 / (2 * RG);  // RG = 2: one tile per pair; RG = 1: two
-            if (step + 1 < 18) {
-#pragma unroll
-              for (int u = 0; u < kTau4 / (2 * RG); ++u) {
-                const KRing& w = kr[(step + 1) % 3][tc + u];
-                if constexpr (FP8) ka[(step + 1) % 2][tc + u] = e4m3x8_bf16((uint32_t)w[0], (uint32_t)w[1]);
+            if (rg == RG - 1 && step + 1 < 18) {
+              const KRing& w = kr[(step + 1) % 3][tau];
+              bf16x8_t& dst = ka[(step + 1) % 2][tau];
+              dst = e4m3x8_bf16((uint32_t)w[0], (uint32_t)w[1]);
+              pin(dst);
+            }
+            if (j == kPer / 2 && (step & 1) == 0 && b_next >= 0) {
+              if constexpr (TOK) {
+                TokIssue8 ti;
+                ti.tok = list[hn * kBlock + 16 * wave + (lane & 15)];
+                ti.buf = (uint32_t)(uintptr_t)next_buf;
+                ti.load(p, step >> 1, wave, lane);
+              } else {
+                issue_load<true>(p, b_next, next_buf, wave, lane, step >> 1);
               }
             }
             __builtin_amdgcn_sched_barrier(0);
           }
           continue;
         }
-        if (step + 1 < 18) key_ops(kr[(step + 1) % 3], ka[(step + 1) % 2]);
-        const bf16x8_t (&ka_s)[kTau4] = ka[step % 2];
-        if (step < 9 && b_next >= 0) {
-          bi.load(p, 2 * step, wave, lane);
-          bi.load(p, 2 * step + 1, wave, lane);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        // bf16: single products, with the key reads of step + 2 (one per
+        // token tile) and this step's loads of the next block between them
+        if constexpr (!FP8) {
         const int ks = step < 2 ? 16 + step : step - 2;
-        bf16x8_t q[RG];
+        constexpr int kPer = RG * kTau4;  // products per step
 #pragma unroll
-        for (int rg = 0; rg < RG; ++rg) q[rg] = qb[rg][ks];
-        if (step == 0) {
-          StGroup<RG, kTau4, true, false, FP8>::run(sacc, ka_s, q);
-        } else if (step == 17 || (kSplitScales && step == 1)) {
-          StGroup<RG, kTau4, false, true, false>::run(sacc, ka_s, q);
-        } else if (kSplitScales && step == 2) {
-          // The RoPE part is complete: weight it by the scale ratio, in place;
-          // the group's lead covers this VALU write of its accumulators.
-#pragma unroll
-          for (int rg = 0; rg < RG; ++rg)
-#pragma unroll
-            for (int tau = 0; tau < kTau4; ++tau) scale_inplace(sacc[rg][tau], pe_ratio);
-          StGroup<RG, kTau4, false, false, true>::run(sacc, ka_s, q);
-        } else {
-          StGroup<RG, kTau4, false, false, false>::run(sacc, ka_s, q);
+        for (int j = 0; j < kPer; ++j) {
+          const int tau = j / RG, rg = j % RG;
+          const bf16x8_t a = kr[step % 3][tau];
+          if (step == 0)
+            st1<true, false>(sacc[rg][tau], a, qb[rg][ks]);
+          else if (step == 17 && j == kPer - 1)
+            st1<false, true>(sacc[rg][tau], a, qb[rg][ks]);
+          else
+            st1<false, false>(sacc[rg][tau], a, qb[rg][ks]);
+          __builtin_amdgcn_sched_barrier(0);
+          // after the products of tile t (RG = 2) or tile t itself (RG = 1):
+          // the read of tile t of step + 2; then the two loads
+          if (rg == RG - 1 && step + 2 < 18) key_frag(step + 2, tau, kr[(step + 2) % 3][tau]);
+          if (step < 9 && b_next >= 0 && j == kPer - 3) bi.load(p, 2 * step, wave, lane);
+          if (step < 9 && b_next >= 0 && j == kPer - 2) bi.load(p, 2 * step + 1, wave, lane);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
 
@@ -1211,6 +1277,7 @@ void partial_kernel(const PartialParams p) {
         // a row that does not attend this entry: no maximum, no weights
         if (((emask >> row_bit[rg]) & 1ull) == 0) bmax[rg] = -INFINITY;
       }
+      m_true[rg] = fmaxf(m_true[rg], bmax[rg]);
       need_any |= bmax[rg] > m_run[rg] + kTau;
     }
     if (__ballot(need_any) != 0) {
@@ -1328,12 +1395,31 @@ void partial_kernel(const PartialParams p) {
       if (g == 0 && row < p.rows) {
         if (direct) {
           const int i = row / p.H, hd = row - (row / p.H) * p.H;
-          p.lse[r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2] = lse;
+          const int64_t lo = r * p.lse_s0 + i * p.lse_s1 + hd * p.lse_s2;
+          if (p.out_wire) {
+            // (m, l): the largest score, and the denominator relative to it
+            // (l_tot is relative to the running maximum, which is at most m)
+            p.lse[lo] = l_tot > 0.f ? m_true[rg] * kLn2 : -INFINITY;
+            p.lse[lo + 1] = l_tot > 0.f ? l_tot * __builtin_amdgcn_exp2f(m_run[rg] - m_true[rg]) : 0.f;
+          } else {
+            p.lse[lo] = lse;
+          }
         } else {
           p.ws_lse[part * p.rows + row] = lse;
+          if (p.out_wire) p.ws_max[part * p.rows + row] = m_true[rg];
         }
       }
-      if (row < p.rows) {
+      if (row < p.rows && direct && p.out_wire) {
+        // bf16 rows: 8-byte runs per row and instruction
+        const int i = row / p.H, hd = row - (row / p.H) * p.H;
+        uint16_t* dst = p.out16 + r * p.out_s0 + i * p.out_s1 + hd * p.out_s2;
+#pragma unroll
+        for (int dt = 0; dt < 32; ++dt) {
+          f32x4_t v = O[dt][rg];
+          asm volatile("" : "+a"(v));  // read in place, no copy back
+          *(u16x4_t*)(dst + 4 * (4 * dt + g)) = f32x4_bf16(v * inv);
+        }
+      } else if (row < p.rows) {
         float* dst;
         if (direct) {
           const int i = row / p.H, hd = row - (row / p.H) * p.H;
@@ -1365,6 +1451,7 @@ void partial_kernel(const PartialParams p) {
     if (g == 0 && row < p.rows) {
       p.ws_lse[part * p.rows + row] = lse;
       p.ws_scale[part * p.rows + row] = row_scale;
+      if (p.out_wire) p.ws_max[part * p.rows + row] = m_true[rg];
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     // lane ln stores 16-byte chunk ln of row rr's 1 KiB fp16 row: columns

@@ -73,7 +73,10 @@ PAPER_COST_MODEL = dict(probe_us=16.0, route_bw_gbs=25.0, compute_us=0.0, merge_
 
 class PartialOpts(ctypes.Structure):
     _fields_ = [("n_splits", ctypes.c_int32), ("row_tile", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 6)]
+                ("out_format", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
+
+
+OUT_FP32, OUT_BF16_WIRE = 0, 1
 
 
 _lib = None
@@ -198,17 +201,20 @@ class _Prepared:
 
 
 def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
-                  out_lat, out_lse, ckv_scale, kpe_scale, n_splits, row_tile, stream):
+                  out_lat, out_lse, ckv_scale, kpe_scale, n_splits, row_tile, stream, wire=False):
     R, Mq, H, _ = q_lat.shape
     if out_lat is None:
-        out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.float32, device=q_lat.device)
+        out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.bfloat16 if wire else torch.float32,
+                              device=q_lat.device)
     if out_lse is None:
-        out_lse = torch.empty((R, Mq, H), dtype=torch.float32, device=q_lat.device)
+        out_lse = torch.empty((R, Mq, H, 2) if wire else (R, Mq, H), dtype=torch.float32,
+                              device=q_lat.device)
     _on_one_gpu(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, out_lat,
                 out_lse, ckv_scale, kpe_scale)
     opts = PartialOpts()
     opts.n_splits = int(n_splits)
     opts.row_tile = int(row_tile)
+    opts.out_format = OUT_BF16_WIRE if wire else OUT_FP32
     descs = (describe(q_lat), describe(q_pe), describe(ckv_pool, ckv_scale),
              describe(kpe_pool, kpe_scale), describe(chunk_block_table), describe(sel_block_ids))
     outs = (describe(out_lat), describe(out_lse))
@@ -229,32 +235,35 @@ def _partial_fn(lib, tokens, no_alloc):
 
 def prepare_partial(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                     out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None, n_splits=0,
-                    row_tile=0, stream=None, tokens=False, no_alloc=False):
+                    row_tile=0, stream=None, tokens=False, no_alloc=False, wire=False):
     """sparse_partial_attn with every argument fixed, the stream included
     (the current one when None); calling the result launches the work and
     returns (out_lat, out_lse)."""
     args, keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                        sel_block_ids, scale, out_lat, out_lse, ckv_scale,
-                                       kpe_scale, n_splits, row_tile, stream)
+                                       kpe_scale, n_splits, row_tile, stream, wire)
     lib = load()
     return _Prepared(_partial_fn(lib, tokens, no_alloc), args, keep, result)
 
 
 def sparse_partial_attn(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids,
                         scale, out_lat=None, out_lse=None, ckv_scale=None, kpe_scale=None,
-                        n_splits=0, row_tile=0, stream=None, tokens=False, no_alloc=False):
+                        n_splits=0, row_tile=0, stream=None, tokens=False, no_alloc=False,
+                        wire=False):
     """Partial attention of each job's Mq x H rows over its selected blocks,
     or with tokens=True over its selected single tokens (sel_block_ids then
     holds logical token ids, block * 64 + t).  no_alloc=True calls the
     allocation-free entry point (split-K partials in the library's static
-    scratch array; block selections only).
+    scratch array; block selections only).  wire=True asks for the bf16
+    wire form of Section 3.2.
 
-    Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]).
+    Returns (out_lat fp32 [R, Mq, H, 512], out_lse fp32 [R, Mq, H]), or with
+    wire=True (out_lat bf16 [R, Mq, H, 512], (m, l) pairs fp32 [R, Mq, H, 2]).
     """
     lib = load()
     args, _keep, result = _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table,
                                         sel_block_ids, scale, out_lat, out_lse, ckv_scale,
-                                        kpe_scale, n_splits, row_tile, stream)
+                                        kpe_scale, n_splits, row_tile, stream, wire)
     _check(lib, _partial_fn(lib, tokens, no_alloc)(*args))
     return result
 
@@ -311,10 +320,11 @@ def _merge_args(parts_lat, parts_lse, out, out_lse, stream):
     if n != len(parts_lse):
         raise ValueError("parts_lat and parts_lse differ in length")
     want_lse = out_lse is not None
-    if out is None:
-        out = torch.empty_like(parts_lat[0])
+    if out is None:  # fp32 whatever form the parts take
+        out = torch.empty(parts_lat[0].shape, dtype=torch.float32, device=parts_lat[0].device)
     if out_lse is True:
-        out_lse = torch.empty_like(parts_lse[0])
+        out_lse = torch.empty(parts_lse[0].shape[:3], dtype=torch.float32,
+                              device=parts_lse[0].device)
     _on_one_gpu(*parts_lat, *parts_lse, out, out_lse if want_lse else None)
     d_lat = [describe(t) for t in parts_lat]
     d_lse = [describe(t) for t in parts_lse]
@@ -334,7 +344,8 @@ def prepare_merge(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
 
 
 def merge_partials(parts_lat, parts_lse, out=None, out_lse=None, stream=None):
-    """LSE merge of partials (lists of [B, Mq, H, 512] / [B, Mq, H] fp32).
+    """LSE merge of partials (lists of [B, Mq, H, 512] / [B, Mq, H] fp32, or
+    of wire-form parts: [B, Mq, H, 512] bf16 / [B, Mq, H, 2] (m, l) fp32).
 
     Returns out (and the merged lse when out_lse is given or requested by
     passing out_lse=True)."""

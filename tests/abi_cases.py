@@ -247,9 +247,15 @@ def merge_cases(device):
         ("part strides differ", lambda a: a["lat"].__setitem__(1, _strided_rows((2, 1, 8, 512), f32,
                                                                                 device, 4)),
          UNSUPPORTED, "strides"),
-        ("part bf16", lambda a: a["lat"].__setitem__(0, torch.zeros((2, 1, 8, 512), dtype=torch.bfloat16,
-                                                                    device=device)), INVALID,
-         "wrong dtype"),
+        # part 0's dtype picks the form (fp32, or the bf16 wire form): a bf16
+        # part after an fp32 one mixes the two
+        ("parts mix fp32 and bf16", lambda a: a["lat"].__setitem__(1, torch.zeros((2, 1, 8, 512),
+                                                                                  dtype=torch.bfloat16,
+                                                                                  device=device)),
+         INVALID, "wrong dtype"),
+        ("wire part with a [B, Mq, H] lse", lambda a: a["lat"].__setitem__(
+            0, torch.zeros((2, 1, 8, 512), dtype=torch.bfloat16, device=device)), INVALID,
+         "expected 4 dims"),
         ("out last dim 511", lambda a: a.update(out=_fill(z(2, 1, 8, 511))), INVALID, "512"),
         ("out rows misaligned", lambda a: a.update(out=_fill(_strided_rows((2, 1, 8, 512), f32, device, 2))),
          INVALID, "16-byte aligned"),
