@@ -406,6 +406,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     p.n_splits = (int32_t)S;
     p.slots_per_split = (int32_t)sps;
     p.split_by_id = by_id ? 1 : 0;
+    // split-major numbering once a split's row tiles fill an XCD's share of
+    // the grid (below that the combine's reads of a tile's splits on one XCD
+    // are worth more than the shared block loads)
+    p.tiles_fast = by_id && row_tiles >= 8 ? 1 : 0;
     p.row_tiles = (int32_t)row_tiles;
     p.scale_log2 = (float)((double)scale * 1.4426950408889634074);
     p.out_wire = wire ? 1 : 0;
@@ -421,7 +425,13 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       // tens of MB; small workspaces keep fp32 rows, whose epilogue and
       // combine are a little shorter (the latency-bound case)
       const size_t n_part_rows = (size_t)R * S * rows;
-      p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
+      // fp16 rows also for per-row block splits of at least 16 MiB whose
+      // splits are long (about 8 blocks or more): there the halved round
+      // trip outweighs the longer epilogue
+      const size_t ws32 = n_part_rows * MLA_DLAT * sizeof(float);
+      p.ws_f16 = ws32 >= (size_t)mla::kWsHalfMinBytes ||
+                 (by_id && ws32 >= ((size_t)16 << 20) &&
+                  std::min<int64_t>(NB, K * tile_qrows) >= 8 * S);
       const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
       const size_t ws_bytes = o_bytes + 3 * n_part_rows * sizeof(float);
       void* ws = nullptr;

@@ -38,6 +38,9 @@ struct PartialParams {
   // per-row selections split by logical block instead of by slot range: split
   // s takes blocks s, s + n_splits, ... from all K slots of every row
   int32_t split_by_id;
+  // work items numbered row tiles fastest (per-row selections split by
+  // logical block, with enough row tiles that one split's tiles fill an XCD)
+  int32_t tiles_fast;
   float scale_log2;  // softmax scale * log2(e)
   // destination: direct (n_splits == 1) or split-K workspace.  out_wire: the
   // bf16 wire form (Section 3.2): bf16 rows at out16 (element strides out_s*)

@@ -881,11 +881,17 @@ void partial_kernel(const PartialParams p) {
   // ---- work item.  Workgroups go to the 8 XCDs round-robin; the ids are
   // renumbered so that each XCD takes one contiguous range.  The splits of a
   // row tile then run on one XCD, and the combine, renumbered alike, reads
-  // their rows on that XCD when both grids split the rows alike.
+  // their rows on that XCD when both grids split the rows alike.  Per-row
+  // selections split by logical block over many row tiles are numbered the
+  // other way round (row tiles fastest): every tile's split s reads blocks
+  // of the same residue class, which then meet in the L2 of one or two XCDs
+  // instead of all eight (the query rows, read once per split, are what is
+  // fetched more than once instead, the smaller of the two).
   const int w_id = gridDim.x % 8 ? (int)blockIdx.x
                                  : (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
-  const int s_idx = w_id % p.n_splits;
-  const int rt = (w_id / p.n_splits) % p.row_tiles;
+  const bool tiles_fast = PR && p.tiles_fast;
+  const int s_idx = tiles_fast ? (w_id / p.row_tiles) % p.n_splits : w_id % p.n_splits;
+  const int rt = tiles_fast ? w_id % p.row_tiles : (w_id / p.n_splits) % p.row_tiles;
   const int r = w_id / (p.n_splits * p.row_tiles);
   const int slot0 = s_idx * p.slots_per_split;
   const int nslots = max(0, min(p.K - slot0, p.slots_per_split));
