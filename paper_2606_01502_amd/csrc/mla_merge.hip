@@ -1,184 +1,20 @@
 // Log-sum-exp merge of partial attention outputs (the requester's online
 // softmax recombination, paper Sections 2.2, 3.3 and 4.2), and the split-K
 // combine that applies the same algebra to one job's slot-range partials.
-//
-// Per row, over the live parts (lse != -inf):
-//   L = max lse_j,  lse = L + ln sum exp(lse_j - L),  out = sum exp(lse_j - lse) o_j.
-// A part with lse = -inf is skipped (its o is never read, so a NaN there
-// cannot leak); no live part gives out = 0, lse = -inf.
-//
-// HBM-bound: one wave per row.  The wave reads the row's part lse values
-// lane-parallel (lane j holds part j), reduces max and sum across the wave,
-// and then visits only the live parts, eight at a time, with each lane moving
-// two 16-byte vectors per part (columns 4*lane and 256 + 4*lane), so that
-// sixteen loads per lane are in flight instead of one part at a time.
+// Both run the row routine of mla_rowmerge.h: HBM-bound, one wave per row.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "mla_kernels.h"
+#include "mla_rowmerge.h"
 
 namespace mla {
 namespace {
 
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
+using namespace rowmerge;
 
 constexpr int kRowsPerBlock = kThreads / 64;  // one wave per row
-constexpr int kBatch = 8;                    // parts in flight per wave
-
-// Reductions over the 64 lanes of a wave, all in VGPRs: the gfx950 row-swap
-// permutes pair lane l with l ^ 32 and then with l ^ 16 (with both operands
-// holding v, the two results at a lane are v[l] and its partner's value);
-// row rotations by 8, 4, 2 and 1 lanes (DPP) then cover the 16 lanes of a
-// row.  Every lane ends with the same value: each step combines the same two
-// values at both lanes of a pair, in either order.
-template <typename Op>
-__device__ __forceinline__ float wave_reduce(float v, Op op) {
-  uint32_t u = __float_as_uint(v);
-  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  v = op(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  u = __float_as_uint(v);
-  const auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  v = op(__uint_as_float(b[0]), __uint_as_float(b[1]));
-  // DPP row_ror:n = 0x120 + n
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false)));
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false)));
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xf, 0xf, false)));
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xf, 0xf, false)));
-  return v;
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-  return wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-  return wave_reduce(v, [](float x, float y) { return x + y; });
-}
-
-// A lane's value read by every lane (src wave-uniform).
-__device__ __forceinline__ float lane_value(float v, int src) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
-}
-
-// Part rows as fp32 (callers' partials) or as fp16 divided by a per-row
-// scale (the split-K workspace): columns 4 lane .. +3 and 256 + 4 lane .. +3.
-struct F32Rows {
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const float* r = row_at(j);
-    v0 = *(const f32x4_t*)(r + 4 * lane);
-    v1 = *(const f32x4_t*)(r + 256 + 4 * lane);
-  }
-};
-
-typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
-typedef uint16_t u16x4_t __attribute__((ext_vector_type(4)));
-
-// bf16 -> fp32 is exact: the bf16 bits are the upper half of the fp32 bits.
-__device__ __forceinline__ f32x4_t bf16x4_f32(u16x4_t a) {
-  return f32x4_t{__uint_as_float((uint32_t)a[0] << 16), __uint_as_float((uint32_t)a[1] << 16),
-                 __uint_as_float((uint32_t)a[2] << 16), __uint_as_float((uint32_t)a[3] << 16)};
-}
-
-// Rows of wire-form parts: bf16.
-struct Bf16Rows {
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const uint16_t* r = row_at(j);
-    v0 = bf16x4_f32(*(const u16x4_t*)(r + 4 * lane));
-    v1 = bf16x4_f32(*(const u16x4_t*)(r + 256 + 4 * lane));
-  }
-};
-
-struct F16Rows {
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const uint16_t* r = row_at(j);
-    const f16x4_t a = *(const f16x4_t*)(r + 4 * lane);
-    const f16x4_t b = *(const f16x4_t*)(r + 256 + 4 * lane);
-    v0 = f32x4_t{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
-    v1 = f32x4_t{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
-  }
-};
-
-// Merge n parts of one row.  lse_at(j): part j's lse; row_at(j): part j's
-// row (Rows says how to read it); scale_at(j): the factor part j's stored
-// values carry (1 for fp32 parts).  Leaves the lane's outputs (columns
-// 4 lane .. +3 and 256 + 4 lane .. +3) in acc0, acc1 and returns the merged
-// lse.
-template <typename Rows, typename LseAt, typename RowAt, typename ScaleAt>
-__device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, ScaleAt scale_at,
-                                           f32x4_t& acc0, f32x4_t& acc1, int lane) {
-  float m = -INFINITY;
-  for (int j0 = 0; j0 < n; j0 += 64) {
-    const int j = j0 + lane;
-    if (j < n) m = fmaxf(m, lse_at(j));
-  }
-  m = wave_max(m);
-  acc0 = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  acc1 = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float lse = -INFINITY;
-  if (m != -INFINITY) {
-    float s = 0.f;
-    for (int j0 = 0; j0 < n; j0 += 64) {
-      const int j = j0 + lane;
-      const float l = j < n ? lse_at(j) : -INFINITY;
-      if (l != -INFINITY) s += __expf(l - m);
-    }
-    lse = m + __logf(wave_sum(s));
-    for (int j0 = 0; j0 < n; j0 += 64) {
-      const int j = j0 + lane;
-      const float l = j < n ? lse_at(j) : -INFINITY;
-      const float w = l != -INFINITY ? __expf(l - lse) * scale_at(j) : 0.f;
-      uint64_t live = __ballot(l != -INFINITY);
-      while (live) {
-        int idx[kBatch];
-        int cnt = 0;
-#pragma unroll
-        for (int k = 0; k < kBatch; ++k) {
-          idx[k] = live ? __builtin_ctzll(live) : idx[0];
-          if (live) {
-            live &= live - 1;
-            ++cnt;
-          }
-        }
-        f32x4_t v0[kBatch], v1[kBatch];
-#pragma unroll
-        for (int k = 0; k < kBatch; ++k)
-          if (k < cnt) Rows::load(row_at, j0 + idx[k], lane, v0[k], v1[k]);
-#pragma unroll
-        for (int k = 0; k < kBatch; ++k) {
-          if (k < cnt) {
-            const float wk = lane_value(w, idx[k]);
-            acc0 += wk * v0[k];
-            acc1 += wk * v1[k];
-          }
-        }
-      }
-    }
-  }
-  return lse;
-}
-
-// Stores of a merged row: fp32, or bf16 rounded to nearest even.
-__device__ __forceinline__ void store_row(float* out, f32x4_t acc0, f32x4_t acc1, int lane) {
-  *(f32x4_t*)(out + 4 * lane) = acc0;
-  *(f32x4_t*)(out + 256 + 4 * lane) = acc1;
-}
-
-__device__ __forceinline__ u16x4_t f32x4_bf16(f32x4_t v) {
-  return u16x4_t{__builtin_bit_cast(uint16_t, (__bf16)v[0]), __builtin_bit_cast(uint16_t, (__bf16)v[1]),
-                 __builtin_bit_cast(uint16_t, (__bf16)v[2]), __builtin_bit_cast(uint16_t, (__bf16)v[3])};
-}
-
-__device__ __forceinline__ void store_row(uint16_t* out, f32x4_t acc0, f32x4_t acc1, int lane) {
-  *(u16x4_t*)(out + 4 * lane) = f32x4_bf16(acc0);
-  *(u16x4_t*)(out + 256 + 4 * lane) = f32x4_bf16(acc1);
-}
 
 __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
   const int n_rows = p.B * p.Mq * p.H;
@@ -194,7 +30,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
   float lse;
   if (p.wire) {
     // wire-form parts: lse = m + ln l from the (m, l) pair (-inf when l = 0)
-    lse = merge_row<Bf16Rows>(
+    lse = merge_parts<true, Bf16Rows>(
         p.n_parts,
         [&](int j) {
           const float m = p.lse[j][lo], l = p.lse[j][lo + 1];
@@ -203,7 +39,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeParams p) {
         [&](int j) { return (const uint16_t*)p.o[j] + oo; }, [](int) { return 1.f; }, acc0, acc1,
         lane);
   } else {
-    lse = merge_row<F32Rows>(
+    lse = merge_parts<true, F32Rows>(
         p.n_parts, [&](int j) { return p.lse[j][lo]; },
         [&](int j) { return (const float*)p.o[j] + oo; }, [](int) { return 1.f; }, acc0, acc1, lane);
   }
@@ -223,38 +59,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineParams p
   const int lane = threadIdx.x & 63;
   const int r = grow / p.rows;
   const int row = grow - r * p.rows;
-  const int64_t base = (int64_t)r * p.S * p.rows + row;  // split j of (r, row) at base + j*rows
-  const int i = row / p.H, h = row - (row / p.H) * p.H;
-  const int64_t oo = r * p.out_s0 + i * p.out_s1 + h * p.out_s2;
-  auto lse_at = [&](int j) { return p.ws_lse[base + (int64_t)j * p.rows]; };
-  f32x4_t acc0, acc1;
-  const float lse =
-      p.ws_f16 ? merge_row<F16Rows>(
-                     p.S, lse_at, [&](int j) { return p.ws_o16 + (base + (int64_t)j * p.rows) * kDLat; },
-                     [&](int j) { return p.ws_scale[base + (int64_t)j * p.rows]; }, acc0, acc1, lane)
-               : merge_row<F32Rows>(
-                     p.S, lse_at, [&](int j) { return p.ws_o32 + (base + (int64_t)j * p.rows) * kDLat; },
-                     [](int) { return 1.f; }, acc0, acc1, lane);
-  const int64_t lo = r * p.lse_s0 + i * p.lse_s1 + h * p.lse_s2;
-  if (!p.out_wire) {
-    store_row(p.out + oo, acc0, acc1, lane);
-    if (lane == 0) p.lse[lo] = lse;
-    return;
-  }
-  // wire form: bf16 row, and (m, l) with m the largest score over the splits
-  // (their maxima, log2 units) and l = exp(lse - m)
-  store_row(p.out16 + oo, acc0, acc1, lane);
-  float m2 = -INFINITY;
-  for (int j0 = 0; j0 < p.S; j0 += 64) {
-    const int j = j0 + lane;
-    if (j < p.S) m2 = fmaxf(m2, p.ws_max[base + (int64_t)j * p.rows]);
-  }
-  m2 = wave_max(m2);
-  if (lane == 0) {
-    const float m = m2 * 0.69314718055994530942f;
-    p.lse[lo] = lse == -INFINITY ? -INFINITY : m;
-    p.lse[lo + 1] = lse == -INFINITY ? 0.f : __expf(lse - m);
-  }
+  combine_row(p, p.S, r, row, lane);
 }
 
 }  // namespace
