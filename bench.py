@@ -274,6 +274,36 @@ def main():
         t1 = time.perf_counter()
         partial_d = event_times(stream, [partial], K)
         merge_d = event_times(stream, [merge], K) if merged is not None else [0.0]
+        # The same step with the partials in Section 3.2's wire form (bf16
+        # rows with (m, l), 1032 B per row instead of 2052), as a holder would
+        # ship them: reported beside the fp32 step, not as the value.
+        wire = None
+        if merged is not None:
+            w_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.bfloat16, device=dev)
+            w_ml = torch.empty((R, Mq, H, 2), dtype=torch.float32, device=dev)
+            w_partial = mla.prepare_partial(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"],
+                                            t["sel"], w.scale, w_lat, w_ml, t["ckv_scale"],
+                                            t["kpe_scale"], n_splits=args.n_splits, stream=stream,
+                                            tokens=w.tokens, wire=True)
+            w_merged = torch.empty_like(merged)
+            w_merge = mla.prepare_merge([w_lat[j * n_req:(j + 1) * n_req] for j in range(parts)],
+                                        [w_ml[j * n_req:(j + 1) * n_req] for j in range(parts)],
+                                        out=w_merged, stream=stream)
+            for _ in range(max(args.warmup, 3)):
+                w_partial()
+                w_merge()
+            stream.synchronize()
+            wire = {"step_us": {k: v * 1e3 for k, v in stats_ms(
+                        event_times(stream, [lambda: (w_partial(), w_merge())], K)).items()},
+                    "partial_us": {k: v * 1e3 for k, v in stats_ms(
+                        event_times(stream, [w_partial], K)).items()},
+                    "merge_us": {k: v * 1e3 for k, v in stats_ms(
+                        event_times(stream, [w_merge], K)).items()}}
+            stream.synchronize()
+            wire["merged_max_row_rel_diff_vs_fp32"] = float(G.row_errors(
+                w_merged.cpu().numpy().astype(np.float64),
+                merged.cpu().numpy().astype(np.float64)).max())
+            del w_lat, w_ml, w_merged
         partial()
         merge()  # leave the outputs of one whole step in place
         torch.cuda.synchronize()
@@ -436,6 +466,7 @@ def main():
         "merge_us_stats": ({k: v * 1e3 for k, v in merge_st.items()} if merged is not None
                            else None),
         "merge_roofline": merge_roofline,
+        "wire_form": wire,
         "cold": cold,
         "host_wall_ms_per_step": (t1 - t0) * 1e3 / K,
         "roofline": roofline,
