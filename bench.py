@@ -100,8 +100,18 @@ def counted_traffic(workload, n_splits, kernel="partial_kernel"):
         return None
     with open(path) as f:
         d = json.load(f)
-    fp = code_fingerprint(os.path.join(ROOT, d["source"]))
+    fp = sources_fingerprint(d.get("sources") or [d["source"]])
     return d["traffic_bytes"] if fp == d.get("source_code_fingerprint") else None
+
+
+def sources_fingerprint(sources):
+    """code_fingerprint of one source, or of several (the kernel's file and
+    the headers it includes) combined."""
+    fps = [code_fingerprint(os.path.join(ROOT, s)) for s in sources]
+    if len(fps) == 1:
+        return fps[0]
+    import hashlib
+    return hashlib.sha256("".join(fps).encode()).hexdigest()
 
 
 def algorithmic(w):
