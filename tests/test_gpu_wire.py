@@ -187,3 +187,24 @@ def test_wire_rejections_write_nothing():
         assert torch.equal(o.view(torch.int16) if o.dtype == torch.bfloat16 else o,
                            o0.view(torch.int16) if o0.dtype == torch.bfloat16 else o0), name
         assert torch.equal(l, l0), name
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+def test_wire_through_the_allocation_free_entry_point(fp8):
+    """The wire form through mla_sparse_partial_attn_noalloc (split partials in
+    the static scratch array, the largest score kept beside each split's lse)
+    equals the allocating entry point's wire output bit for bit."""
+    print(f"case: wire no-alloc fp8={fp8}", flush=True)
+    w = W.random_case(311, R=3, Mq=2, H=24, P=20, NB=9, K=7, n_valid=[7, 0, 4])
+    if fp8:
+        w = w.to_fp8(shared_scale=False)
+    t = G.upload(w)
+    for n_splits in (1, 3):
+        o_a, ml_a = _call(t, w, True, n_splits)
+        o_n, ml_n = mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"],
+                                            t["sel"], w.scale, ckv_scale=t["ckv_scale"],
+                                            kpe_scale=t["kpe_scale"], n_splits=n_splits,
+                                            no_alloc=True, wire=True)
+        torch.cuda.synchronize()
+        assert torch.equal(o_a.view(torch.int16), o_n.view(torch.int16)), n_splits
+        assert torch.equal(ml_a, ml_n), n_splits
