@@ -145,126 +145,11 @@ __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 // S^T products with the accumulators in architectural VGPRs.  The compiler
 // selects the accumulation-register form for every MFMA of a kernel that uses
 // accumulation registers at all, and the 256 of them hold O here; these
-// products are therefore written as inline asm with "v" operands.  MFMA
-// results are not interlocked against VALU reads: the final group pads with
-// s_nop (24 wait states, enough for a 16-pass XDL op) before the accumulators
-// are read; accumulators are only ever read by the next group's MFMAs in
-// between (7 independent MFMAs apart), and the first group starts from the
-// literal 0, so no VALU write feeds a product.
-#define MLA_MFMA "v_mfma_f32_16x16x32_bf16 "
-
-// One k-step of S^T for RG row groups x NT token tiles, as one asm statement:
-// c[rg][tau] += a[tau] . q[rg].  kFirst starts from the literal 0; kLast pads
-// with 24 wait states so the results may be read by VALU code (MFMA results
-// are not interlocked against VALU reads).  kPre leads with 3 wait states, for
-// operands just written by VALU code (VALU writes are not interlocked against
-// MFMA reads either).  Accumulators of consecutive groups are RG*NT - 1 >= 3
-// independent products apart.
-template <int RG, int NT, bool kFirst, bool kLast, bool kPre>
-struct StGroup;
-
-#define MLA_NOPS "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
-// RG = 2, NT = 4: %0..%7 accumulators (rg-major), %8..%11 keys, %12..%13 queries
-#define MLA_G24(C) \
-  MLA_MFMA "%0, %8, %12, " C(0) "\n\t" MLA_MFMA "%1, %9, %12, " C(1) "\n\t"    \
-  MLA_MFMA "%2, %10, %12, " C(2) "\n\t" MLA_MFMA "%3, %11, %12, " C(3) "\n\t"  \
-  MLA_MFMA "%4, %8, %13, " C(4) "\n\t" MLA_MFMA "%5, %9, %13, " C(5) "\n\t"    \
-  MLA_MFMA "%6, %10, %13, " C(6) "\n\t" MLA_MFMA "%7, %11, %13, " C(7)
-// RG = 2, NT = 2: %0..%3 accumulators, %4..%5 keys, %6..%7 queries
-#define MLA_G22(C) \
-  MLA_MFMA "%0, %4, %6, " C(0) "\n\t" MLA_MFMA "%1, %5, %6, " C(1) "\n\t" \
-  MLA_MFMA "%2, %4, %7, " C(2) "\n\t" MLA_MFMA "%3, %5, %7, " C(3)
-// RG = 1, NT = 4: %0..%3 accumulators, %4..%7 keys, %8 query
-#define MLA_G14(C) \
-  MLA_MFMA "%0, %4, %8, " C(0) "\n\t" MLA_MFMA "%1, %5, %8, " C(1) "\n\t" \
-  MLA_MFMA "%2, %6, %8, " C(2) "\n\t" MLA_MFMA "%3, %7, %8, " C(3)
-#define MLA_ZERO(i) "0"
-#define MLA_ACC0 "%0"
-#define MLA_ACC1 "%1"
-#define MLA_ACC2 "%2"
-#define MLA_ACC3 "%3"
-#define MLA_ACC4 "%4"
-#define MLA_ACC5 "%5"
-#define MLA_ACC6 "%6"
-#define MLA_ACC7 "%7"
-#define MLA_ACC(i) MLA_ACC##i
-#define MLA_OUT24(m) m(c[0][0]), m(c[0][1]), m(c[0][2]), m(c[0][3]), \
-                     m(c[1][0]), m(c[1][1]), m(c[1][2]), m(c[1][3])
-#define MLA_OUT22(m) m(c[0][0]), m(c[0][1]), m(c[1][0]), m(c[1][1])
-#define MLA_OUT14(m) m(c[0][0]), m(c[0][1]), m(c[0][2]), m(c[0][3])
-#define MLA_W(x) "=&v"(x)
-#define MLA_RW(x) "+v"(x)
-#define MLA_PRE "s_nop 2\n\t"
-#define MLA_STGROUP(RG_, NT_, G, OUTS, ...)                                                 \
-  template <bool kLast, bool kPre>                                                          \
-  struct StGroup<RG_, NT_, true, kLast, kPre> {                                             \
-    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
-                                               const bf16x8_t (&a)[NT_],                    \
-                                               const bf16x8_t (&q)[RG_]) {                  \
-      if constexpr (kPre)                                                                   \
-        asm(MLA_PRE G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                               \
-      else                                                                                  \
-        asm(G(MLA_ZERO) : OUTS(MLA_W) : __VA_ARGS__);                                       \
-    }                                                                                       \
-  };                                                                                        \
-  template <bool kPre>                                                                      \
-  struct StGroup<RG_, NT_, false, false, kPre> {                                            \
-    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
-                                               const bf16x8_t (&a)[NT_],                    \
-                                               const bf16x8_t (&q)[RG_]) {                  \
-      if constexpr (kPre)                                                                   \
-        asm(MLA_PRE G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                               \
-      else                                                                                  \
-        asm(G(MLA_ACC) : OUTS(MLA_RW) : __VA_ARGS__);                                       \
-    }                                                                                       \
-  };                                                                                        \
-  template <bool kPre>                                                                      \
-  struct StGroup<RG_, NT_, false, true, kPre> {                                             \
-    static __device__ __forceinline__ void run(f32x4_t (&c)[RG_][NT_],                      \
-                                               const bf16x8_t (&a)[NT_],                    \
-                                               const bf16x8_t (&q)[RG_]) {                  \
-      if constexpr (kPre)                                                                   \
-        asm(MLA_PRE G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                      \
-      else                                                                                  \
-        asm(G(MLA_ACC) MLA_NOPS : OUTS(MLA_RW) : __VA_ARGS__);                              \
-    }                                                                                       \
-  };
-MLA_STGROUP(2, 4, MLA_G24, MLA_OUT24, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]), "v"(q[1]))
-MLA_STGROUP(2, 2, MLA_G22, MLA_OUT22, "v"(a[0]), "v"(a[1]), "v"(q[0]), "v"(q[1]))
-MLA_STGROUP(1, 4, MLA_G14, MLA_OUT14, "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(q[0]))
-#undef MLA_STGROUP
-#undef MLA_G24
-#undef MLA_G22
-#undef MLA_G14
-#undef MLA_OUT24
-#undef MLA_OUT22
-#undef MLA_OUT14
-#undef MLA_NOPS
-#undef MLA_PRE
-#undef MLA_MFMA
-
-// Two S^T products sharing one query operand, c0 += a0 . q and c1 += a1 . q,
-// as one asm statement (the fp8 path issues a step as four of these with the
-// code conversions of the next step between them).  kFirst, kLast and kPre
-// as for StGroup.
-#define MLA_P2(C0, C1) "v_mfma_f32_16x16x32_bf16 %0, %2, %4, " C0 "\n\tv_mfma_f32_16x16x32_bf16 %1, %3, %4, " C1
-template <bool kFirst, bool kLast, bool kPre>
-__device__ __forceinline__ void st_pair(f32x4_t& c0, f32x4_t& c1, bf16x8_t a0, bf16x8_t a1, bf16x8_t q) {
-  if constexpr (kFirst) {
-    if constexpr (kPre)
-      asm("s_nop 2\n\t" MLA_P2("0", "0") : "=&v"(c0), "=&v"(c1) : "v"(a0), "v"(a1), "v"(q));
-    else
-      asm(MLA_P2("0", "0") : "=&v"(c0), "=&v"(c1) : "v"(a0), "v"(a1), "v"(q));
-  } else if constexpr (kLast) {
-    asm(MLA_P2("%0", "%1") "\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
-  } else if constexpr (kPre) {
-    asm("s_nop 2\n\t" MLA_P2("%0", "%1") : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
-  } else {
-    asm(MLA_P2("%0", "%1") : "+v"(c0), "+v"(c1) : "v"(a0), "v"(a1), "v"(q));
-  }
-}
-#undef MLA_P2
-
+// products are therefore written as inline asm with "v" operands.  Neither
+// direction is interlocked: VALU code may read a product's result only 24
+// wait states (a 16-pass XDL op) after it, and a product may read an operand
+// that VALU code wrote only 3 wait states later.  The build checks the
+// generated code for both (hazards.py).
 // One S^T product, c += a . q (kFirst: c = a . q), as an asm statement of its
 // own.  A wave issues in order and waits at a product until the matrix core
 // takes it, so only what is placed between single products (key reads,
