@@ -104,6 +104,19 @@ def counted_traffic(workload, n_splits, kernel="partial_kernel"):
     return d["traffic_bytes"] if fp == d.get("source_code_fingerprint") else None
 
 
+def counted_flop(workload, n_splits):
+    """Matrix-core FLOP per launch of the partial kernel from the committed
+    rocprofv3 counter summary (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512), or None
+    when there is none for this workload or it is for an older source."""
+    path = os.path.join(ROOT, "profiles", f"partial_kernel_{workload}_mfma.json")
+    if n_splits != 0 or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    fp = sources_fingerprint(d["sources"])
+    return d["flop_per_dispatch"] if fp == d.get("source_code_fingerprint") else None
+
+
 def sources_fingerprint(sources):
     """code_fingerprint of one source, or of several (the kernel's file and
     the headers it includes) combined."""
@@ -431,9 +444,14 @@ def main():
     # The bound is the roofline side the kernel's algorithmic intensity falls
     # on (ridge = bf16 MFMA peak / HBM peak, about 312 FLOP/B).
     traffic = counted_traffic(w.name, args.n_splits)
+    c_flop = counted_flop(w.name, args.n_splits)
     common = {"traffic": traffic, "kernel": "partial_kernel", "algorithmic_bytes": alg_bytes,
               "kv_bytes": kv_bytes, "flops": flops,
-              "intensity_flop_per_byte": flops / alg_bytes}
+              "intensity_flop_per_byte": flops / alg_bytes,
+              # the matrix core's own count of the work (rocprofv3 counter), per
+              # launch, over the same event-timed duration as `achieved`
+              "counter_flop": c_flop,
+              "counter_tflops": c_flop / (partial_ms * 1e-3) / 1e12 if c_flop else None}
     if flops / alg_bytes > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
         roofline = {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": tflops / BF16_PEAK_TFLOPS, **common}
@@ -463,6 +481,7 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8-e4m3 kv, bf16 mfma" if w.fp8 else "bf16",
         "data": "synthetic",
+        "device": {"name": torch.cuda.get_device_name(0), "hip": torch.version.hip},
         "config": {"workload": w.name, "requests": n_req, "jobs": R, "mq": Mq, "heads": H,
                    ("selected_tokens" if w.tokens else "selected_blocks"): int((w.sel >= 0).sum()),
                    "block_tokens": BLOCK,
