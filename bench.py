@@ -481,7 +481,9 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8-e4m3 kv, bf16 mfma" if w.fp8 else "bf16",
         "data": "synthetic",
-        "device": {"name": torch.cuda.get_device_name(0), "hip": torch.version.hip},
+        "device": {"name": torch.cuda.get_device_name(0),
+                   "arch": getattr(torch.cuda.get_device_properties(0), "gcnArchName", None),
+                   "hip": torch.version.hip},
         "config": {"workload": w.name, "requests": n_req, "jobs": R, "mq": Mq, "heads": H,
                    ("selected_tokens" if w.tokens else "selected_blocks"): int((w.sel >= 0).sum()),
                    "block_tokens": BLOCK,

@@ -421,17 +421,11 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     std::unique_lock<std::mutex> ws_lock;  // held until the combine is queued
     if (S > 1) {
       // split rows, then their scales (fp16 rows only), then their lse values.
-      // fp16 rows halve the workspace round trip, which pays once it moves
-      // tens of MB; small workspaces keep fp32 rows, whose epilogue and
-      // combine are a little shorter (the latency-bound case)
+      // fp16 rows halve the workspace round trip, which pays from about a
+      // megabyte of split rows on; tiny workspaces keep fp32 rows, whose
+      // epilogue is a little shorter
       const size_t n_part_rows = (size_t)R * S * rows;
-      // fp16 rows also for per-row block splits of at least 16 MiB whose
-      // splits are long (about 8 blocks or more): there the halved round
-      // trip outweighs the longer epilogue
-      const size_t ws32 = n_part_rows * MLA_DLAT * sizeof(float);
-      p.ws_f16 = ws32 >= (size_t)mla::kWsHalfMinBytes ||
-                 (by_id && ws32 >= ((size_t)16 << 20) &&
-                  std::min<int64_t>(NB, K * tile_qrows) >= 8 * S);
+      p.ws_f16 = n_part_rows * MLA_DLAT * sizeof(float) >= (size_t)mla::kWsHalfMinBytes;
       const size_t o_bytes = n_part_rows * MLA_DLAT * (p.ws_f16 ? sizeof(uint16_t) : sizeof(float));
       const size_t ws_bytes = o_bytes + 3 * n_part_rows * sizeof(float);
       void* ws = nullptr;

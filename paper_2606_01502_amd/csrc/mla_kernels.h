@@ -13,8 +13,9 @@ constexpr int kBlock = 64;   // tokens per cache block
 constexpr int kThreads = 256;             // merge / combine workgroup size
 constexpr int kMaxSlotsPerSplit = 1024;   // selected-slot range one workgroup handles
 constexpr int kMaxParts = 64;
-// split-K workspaces of at least this many fp32 row bytes store fp16 rows
-constexpr int64_t kWsHalfMinBytes = 48ll << 20;
+// split-K workspaces of at least this many fp32 row bytes store scaled fp16
+// rows (below it, as for a handful of rows, the shorter fp32 epilogue pays)
+constexpr int64_t kWsHalfMinBytes = 1ll << 20;
 
 // Partial attention over one (job, row tile, slot range) per workgroup.
 struct PartialParams {

@@ -60,7 +60,9 @@ __device__ __forceinline__ float lane_value(float v, int src) {
 }
 
 // Part rows as fp32 (callers' partials) or as fp16 divided by a per-row
-// scale (the split-K workspace): columns 4 lane .. +3 and 256 + 4 lane .. +3.
+// scale (the split-K workspace): a lane loads columns 4 lane .. +3 and
+// 256 + 4 lane .. +3 as raw values (load_raw) and converts them to fp32 where
+// it uses them (cvt), so that the loads of several parts are in flight at once.
 struct F32Rows {
   typedef f32x4_t Raw;
   template <typename RowAt>
@@ -70,13 +72,6 @@ struct F32Rows {
     v1 = *(const f32x4_t*)(r + 256 + 4 * lane);
   }
   __device__ __forceinline__ static f32x4_t cvt(Raw v) { return v; }
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const float* r = row_at(j);
-    v0 = *(const f32x4_t*)(r + 4 * lane);
-    v1 = *(const f32x4_t*)(r + 256 + 4 * lane);
-  }
 };
 
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
@@ -98,13 +93,6 @@ struct Bf16Rows {
     v1 = *(const u16x4_t*)(r + 256 + 4 * lane);
   }
   __device__ __forceinline__ static f32x4_t cvt(Raw a) { return bf16x4_f32(a); }
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const uint16_t* r = row_at(j);
-    v0 = bf16x4_f32(*(const u16x4_t*)(r + 4 * lane));
-    v1 = bf16x4_f32(*(const u16x4_t*)(r + 256 + 4 * lane));
-  }
 };
 
 struct F16Rows {
@@ -117,15 +105,6 @@ struct F16Rows {
   }
   __device__ __forceinline__ static f32x4_t cvt(Raw a) {
     return f32x4_t{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
-  }
-  template <typename RowAt>
-  __device__ __forceinline__ static void load(RowAt row_at, int j, int lane, f32x4_t& v0,
-                                              f32x4_t& v1) {
-    const uint16_t* r = row_at(j);
-    const f16x4_t a = *(const f16x4_t*)(r + 4 * lane);
-    const f16x4_t b = *(const f16x4_t*)(r + 256 + 4 * lane);
-    v0 = f32x4_t{(float)a[0], (float)a[1], (float)a[2], (float)a[3]};
-    v1 = f32x4_t{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
   }
 };
 
@@ -170,16 +149,17 @@ __device__ __forceinline__ float merge_row(int n, LseAt lse_at, RowAt row_at, Sc
             ++cnt;
           }
         }
-        f32x4_t v0[kBatch], v1[kBatch];
+        // raw values first (converted at use), so that no load waits for another
+        typename Rows::Raw v0[kBatch], v1[kBatch];
 #pragma unroll
         for (int k = 0; k < kBatch; ++k)
-          if (k < cnt) Rows::load(row_at, j0 + idx[k], lane, v0[k], v1[k]);
+          if (k < cnt) Rows::load_raw(row_at, j0 + idx[k], lane, v0[k], v1[k]);
 #pragma unroll
         for (int k = 0; k < kBatch; ++k) {
           if (k < cnt) {
             const float wk = lane_value(w, idx[k]);
-            acc0 += wk * v0[k];
-            acc1 += wk * v1[k];
+            acc0 += wk * Rows::cvt(v0[k]);
+            acc1 += wk * Rows::cvt(v1[k]);
           }
         }
       }

@@ -119,7 +119,7 @@ def test_graph_replay_tokens_fp8_and_fetch():
             stream.synchronize()
             for a, b in zip(outs, ref):
                 assert torch.equal(a, b), f"replay {rep} differs from the eager result"
-            # eager work of another size on the same stream (fp32 workspace rows)
+            # eager work of another size on the same stream (another split plan)
             mla.sparse_partial_attn(t["q_lat"][:2], t["q_pe"][:2], t["ckv"], t["kpe"],
                                     t["table"][:2], t["sel"][:2], w.scale,
                                     ckv_scale=t["ckv_scale"], kpe_scale=t["kpe_scale"],
