@@ -204,7 +204,9 @@ mla_status_t mla_sparse_partial_attn_ex(const mla_tensor_t* q_lat, const mla_ten
  * holds on each GPU it runs on until the process ends, instead of memory it
  * allocates.  The call allocates nothing (no hipMalloc, no allocating library
  * routine).  A call whose split partials need more than the array (about
- * 32K partial rows: jobs x row tiles x splits x 128 rows) returns
+ * 64K partial rows, jobs x row tiles x splits x 128 rows, once they are
+ * stored as scaled fp16, which they are from a megabyte of fp32 rows on;
+ * about 32K below that) returns
  * MLA_ERR_UNSUPPORTED before anything is enqueued.  Every call on one GPU
  * shares that GPU's array: calls that overlap in time on one GPU (on
  * different streams, or from graphs replayed concurrently) race on it and

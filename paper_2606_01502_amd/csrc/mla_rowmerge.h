@@ -192,7 +192,8 @@ __device__ __forceinline__ void store_row(uint16_t* out, f32x4_t acc0, f32x4_t a
 // but never enter the sum: with kGuard (callers' parts, which may hold NaN
 // there) a part is added only when live; without it (the split-K workspace,
 // whose rows are always finite) a dead part is added with weight 0.  Same
-// arithmetic and order as merge_row.
+// arithmetic and order as merge_row.  n >= 1 (the merge takes 1..64 parts,
+// the combine two splits or more).
 template <int N, bool kGuard, typename Rows, typename LseAt, typename RowAt, typename ScaleAt>
 __device__ __forceinline__ float merge_row_one_trip(int n, LseAt lse_at, RowAt row_at,
                                                     ScaleAt scale_at, f32x4_t& acc0,
