@@ -54,8 +54,8 @@ struct PartialParams {
   float* lse;
   int64_t lse_s0, lse_s1, lse_s2;
   // split-K workspace, [R][S][rows] split rows with their lse: fp32 rows, or
-  // when ws_f16 is set (large workspaces) fp16 rows divided by the row's
-  // largest magnitude, which ws_scale holds
+  // when ws_f16 is set (a megabyte of fp32 rows or more) fp16 rows divided
+  // by the row's largest magnitude, which ws_scale holds
   int32_t ws_f16;
   float* ws_o32;     // [R][S][rows][512]
   uint16_t* ws_o16;  // [R][S][rows][512] fp16 bits

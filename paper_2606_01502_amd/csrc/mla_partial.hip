@@ -43,8 +43,8 @@
 // rows' blocks once and masks every row to its own multiset; or single
 // tokens (an indexer's top-k, Section 6.3's selection budgets), gathered 64
 // at a time into the same stage layout, each with its own block's fp8
-// scales.  Splits of a large workspace store their rows as fp16 scaled by the
-// row's largest magnitude.
+// scales.  Splits of a workspace of a megabyte or more store their rows as
+// fp16 scaled by the row's largest magnitude.
 //
 // LDS swizzles (token t of the block, 16-byte chunk c of its row) are
 // described with bf16_key and fp8_key below.
@@ -1264,9 +1264,10 @@ void partial_kernel(const PartialParams p) {
   // n16 for every column tile dt: fp32 rows are stored straight from there
   // (64-byte runs per row and instruction, which the L2 joins into whole
   // lines; measured faster than transposing through LDS first).  Splits of a
-  // large workspace write their rows as fp16 values divided by the row's
-  // largest magnitude (kept in fp32 beside the lse): half the bytes of fp32,
-  // at 2^-11 of that magnitude, which the combine multiplies back; those
+  // workspace of a megabyte or more write their rows as fp16 values divided
+  // by the row's largest magnitude (kept in fp32 beside the lse): half the
+  // bytes of fp32, at 2^-11 of that magnitude, which the combine multiplies
+  // back; those
   // rows are transposed through LDS (a 32 KiB area per wave, 16-byte chunk c
   // of row rr in slot c ^ rr) and stored as contiguous 1 KiB rows.
   const bool direct = p.n_splits == 1;
