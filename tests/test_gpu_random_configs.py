@@ -1,8 +1,9 @@
 """Randomised configurations against the oracle: every combination of cache
 type (bf16, fp8 with one or two scale arrays) and selection mode (blocks,
 tokens, per-row blocks), with random job counts, rows, heads, slot counts,
-padding, duplicates, split counts and row tiles.  The draws are seeded, so
-each case is reproducible from its index."""
+padding, duplicates, split counts and row tiles, and every fourth draw again
+with the wire-form output.  The draws are seeded, so each case is
+reproducible from its index."""
 import numpy as np
 import pytest
 
@@ -57,3 +58,16 @@ def test_random_config(i):
     ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
                                   w.ckv_scale, w.kpe_scale, tokens=w.tokens)
     G.assert_parity(out, lse, ref_o, ref_l, f"random case {i}")
+
+
+@pytest.mark.parametrize("i", range(0, N_CASES, 4))
+def test_random_config_wire(i):
+    """The same draws with the output in Section 3.2's wire form: bf16 rows
+    bit-exact against the fp32 form rounded, (m, l) against the oracle."""
+    from tests.test_gpu_wire import _check_wire
+    cache, mode, kw, n_splits, row_tile = _draw(i)
+    print(f"case {i} wire: {cache} {mode} {kw} splits={n_splits} row_tile={row_tile}", flush=True)
+    w = W.random_case(9000 + i, **kw)
+    if cache != "bf16":
+        w = w.to_fp8(shared_scale=cache == "fp8")
+    _check_wire(w, n_splits, row_tile=row_tile, what=f"random case {i} wire")
