@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define MLA_SPARSE_VERSION 3
+#define MLA_SPARSE_VERSION 4
 
 #define MLA_DLAT 512  /* latent width = d_v (Section 3.2)                    */
 #define MLA_DPE 64    /* decoupled-RoPE width = d_qk - d_v (Section 3.2)      */
@@ -82,9 +82,15 @@ typedef struct {
  * 3.3, 6.3).  R independent jobs (one per (request, chunk)); job r has
  * Mq x H query rows that all share one selection of 64-token blocks.
  *
- *   q_lat             [R, Mq, H, 512] bf16   latent part of the absorbed query
- *   q_pe              [R, Mq, H, 64]  bf16   decoupled-RoPE part (already rotated
+ *   q_lat             [R_q, Mq, H, 512] bf16 latent part of the absorbed query
+ *   q_pe              [R_q, Mq, H, 64]  bf16 decoupled-RoPE part (already rotated
  *                                            by the requester; no rotation here)
+ *                                     R_q = R (a q per job), or any R_q dividing
+ *                                     R: job r then reads q row r mod R_q, so a
+ *                                     request routed to several chunks of this
+ *                                     holder (jobs b, b + R_q, ... in slot-major
+ *                                     order) sends its q once; those jobs are
+ *                                     scheduled next to each other
  *   ckv_pool          [P, 64, 512]    bf16 or fp8-e4m3fn (+block_scale), contiguous
  *   kpe_pool          [P, 64, 64]     same dtype as ckv_pool, contiguous
  *                                     fp8: both descriptors carry a block_scale;

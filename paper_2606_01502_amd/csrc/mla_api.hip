@@ -242,7 +242,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
         return fail(MLA_ERR_INVALID_ARGUMENT, "opts.row_tile must be 0, 64 or 128");
     }
 
-    const int64_t R = q_lat->shape[0], Mq = q_lat->shape[1], H = q_lat->shape[2];
+    // jobs come from the block table; q may hold fewer rows, R_q dividing R,
+    // job r reading q row r mod R_q (one request's q shared by its chunks)
+    const int64_t R = chunk_block_table->shape[0];
+    const int64_t Rq = q_lat->shape[0], Mq = q_lat->shape[1], H = q_lat->shape[2];
     const int64_t P = ckv_pool->shape[0];
     const int64_t NB = chunk_block_table->shape[1], K = sel_block_ids->shape[per_row ? 2 : 1];
     auto shape_is = [](const mla_tensor_t* t, std::initializer_list<int64_t> s) {
@@ -252,7 +255,10 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
       return true;
     };
     if (q_lat->shape[3] != MLA_DLAT) return fail(MLA_ERR_INVALID_ARGUMENT, "q_lat: last dim must be 512");
-    if (!shape_is(q_pe, {R, Mq, H, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "q_pe: shape must be [R, Mq, H, 64]");
+    if (R > 0 ? (Rq < 1 || R % Rq != 0) : Rq != 0)
+      return fail(MLA_ERR_INVALID_ARGUMENT,
+                  "q_lat: its first dim R_q must divide the number of jobs R (job r reads q row r mod R_q)");
+    if (!shape_is(q_pe, {Rq, Mq, H, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "q_pe: shape must be [R_q, Mq, H, 64]");
     if (!shape_is(ckv_pool, {P, MLA_BLOCK, MLA_DLAT})) return fail(MLA_ERR_INVALID_ARGUMENT, "ckv_pool: shape must be [P, 64, 512]");
     if (!shape_is(kpe_pool, {P, MLA_BLOCK, MLA_DPE})) return fail(MLA_ERR_INVALID_ARGUMENT, "kpe_pool: shape must be [P, 64, 64] with the P of ckv_pool");
     if (chunk_block_table->shape[0] != R) return fail(MLA_ERR_INVALID_ARGUMENT, "chunk_block_table: shape must be [R, NB]");
@@ -410,6 +416,8 @@ mla_status_t partial_call(const mla_tensor_t* q_lat, const mla_tensor_t* q_pe,
     p.n_splits = (int32_t)S;
     p.slots_per_split = (int32_t)sps;
     p.split_by_id = by_id ? 1 : 0;
+    p.q_jobs = (int32_t)std::max<int64_t>(Rq, 1);
+    p.q_rep = (int32_t)(Rq > 0 ? R / Rq : 1);
     // split-major numbering once a split's row tiles fill an XCD's share of
     // the grid (below that the combine's reads of a tile's splits on one XCD
     // are worth more than the shared block loads)

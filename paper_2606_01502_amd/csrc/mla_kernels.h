@@ -39,6 +39,10 @@ struct PartialParams {
   // per-row selections split by logical block instead of by slot range: split
   // s takes blocks s, s + n_splits, ... from all K slots of every row
   int32_t split_by_id;
+  // q rows shared by jobs: job r reads q row r % q_jobs; with q_rep =
+  // jobs / q_jobs > 1 the work items of one q row's jobs are numbered next to
+  // each other (so that they run on one XCD and read that row from one L2)
+  int32_t q_jobs, q_rep;
   // work items numbered row tiles fastest (per-row selections split by
   // logical block, with enough row tiles that one split's tiles fill an XCD)
   int32_t tiles_fast;

@@ -777,7 +777,10 @@ void partial_kernel(const PartialParams p) {
   const bool tiles_fast = PR && p.tiles_fast;
   const int s_idx = tiles_fast ? (w_id / p.row_tiles) % p.n_splits : w_id % p.n_splits;
   const int rt = tiles_fast ? w_id % p.row_tiles : (w_id / p.n_splits) % p.row_tiles;
-  const int r = w_id / (p.n_splits * p.row_tiles);
+  const int r_num = w_id / (p.n_splits * p.row_tiles);
+  // jobs that share q rows (r, r + q_jobs, ...) take consecutive numbers
+  const int r = p.q_rep > 1 ? (r_num % p.q_rep) * p.q_jobs + r_num / p.q_rep : r_num;
+  const int rq = r % p.q_jobs;  // the job's q rows
   const int slot0 = s_idx * p.slots_per_split;
   const int nslots = max(0, min(p.K - slot0, p.slots_per_split));
 
@@ -817,8 +820,8 @@ void partial_kernel(const PartialParams p) {
     const int row = row_wg0 + wave * 16 * RG + rg * 16 + n16;
     if (row < p.rows) {
       const int i = row / p.H, h = row - (row / p.H) * p.H;
-      const uint16_t* ql = p.q_lat + r * p.ql_s0 + i * p.ql_s1 + h * p.ql_s2 + g * 8;
-      const uint16_t* qp = p.q_pe + r * p.qp_s0 + i * p.qp_s1 + h * p.qp_s2 + g * 8;
+      const uint16_t* ql = p.q_lat + rq * p.ql_s0 + i * p.ql_s1 + h * p.ql_s2 + g * 8;
+      const uint16_t* qp = p.q_pe + rq * p.qp_s0 + i * p.qp_s1 + h * p.qp_s2 + g * 8;
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks) qb[rg][ks] = *(const bf16x8_t*)(ql + ks * 32);
 #pragma unroll

@@ -202,7 +202,8 @@ class _Prepared:
 
 def _partial_args(q_lat, q_pe, ckv_pool, kpe_pool, chunk_block_table, sel_block_ids, scale,
                   out_lat, out_lse, ckv_scale, kpe_scale, n_splits, row_tile, stream, wire=False):
-    R, Mq, H, _ = q_lat.shape
+    R = chunk_block_table.shape[0]  # jobs; q may hold fewer rows (R_q dividing R)
+    _, Mq, H, _ = q_lat.shape
     if out_lat is None:
         out_lat = torch.empty((R, Mq, H, DLAT), dtype=torch.bfloat16 if wire else torch.float32,
                               device=q_lat.device)

@@ -271,9 +271,11 @@ def batched_merge(seed=3, n_requests=64, n_chunks=256, chunk_blocks=128, hits=4,
                                  .reshape(R, 1, 128, DLAT))
     q_pe = np.ascontiguousarray(np.broadcast_to(q_req_pe[None], (hits,) + q_req_pe.shape)
                                 .reshape(R, 1, 128, DPE))
+    # (the q of job j * n_requests + b is request b's: the first n_requests
+    # rows hold every distinct q, which a holder needs only once)
     return Workload("batched-merge", q_lat, q_pe, ckv, kpe, table, sel,
                     n_requests=n_requests, merge_parts=hits,
-                    meta=dict(chunks=chunks))
+                    meta=dict(chunks=chunks, q_rows=n_requests))
 
 
 def zipf_ids(rng, n, k, a=1.1):

@@ -128,7 +128,11 @@ def partial_cases(device):
         ("q_pe R differs", lambda a: a.update(q_pe=z(3, 3, 16, 64)), INVALID, "q_pe: shape"),
         ("out_lat H differs", lambda a: a.update(out_lat=_fill(z(2, 3, 8, 512, dt=f32))), INVALID,
          "out_lat: shape"),
-        ("table R differs", lambda a: a.update(table=z(3, 5, dt=i32)), INVALID, "chunk_block_table"),
+        # jobs come from the table: q's 2 rows must divide them
+        ("table R not a multiple of q rows", lambda a: a.update(table=z(3, 5, dt=i32)), INVALID,
+         "divide"),
+        ("table R twice q rows, sel not", lambda a: a.update(table=z(4, 5, dt=i32)), INVALID,
+         "sel_block_ids: shape"),
         ("kpe P differs", lambda a: a.update(kpe=z(9, 64, 64)), INVALID, "kpe_pool: shape"),
         ("q_lat inner stride 2", lambda a: a.update(q_lat=z(2, 3, 16, 1024)[..., ::2]), INVALID,
          "innermost stride"),

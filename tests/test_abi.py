@@ -33,7 +33,7 @@ def test_version_and_error_string_without_gpu():
     lib = mla.load()
     with open(os.path.join(ROOT, "include", "mla_sparse.h")) as f:
         want = int(re.search(r"#define MLA_SPARSE_VERSION (\d+)", f.read()).group(1))
-    assert lib.mla_version() == want == 3
+    assert lib.mla_version() == want == 4
     assert lib.mla_last_error() == b""
 
 

@@ -240,3 +240,41 @@ def test_dense_local_bf16_config_sampled():
     ref_o, ref_l = _oracle(w, jobs)
     rel, lerr = G.assert_parity(out[jobs], lse[jobs], ref_o, ref_l, "dense-local bf16")
     print(f"dense-local bf16: max row-rel {rel:.3g}, max lse {lerr:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("mode", ["blocks", "tokens", "per_row"])
+@pytest.mark.parametrize("n_splits", [0, 2])
+def test_shared_q_rows(mode, n_splits):
+    """q with R_q < R rows: job r reads q row r mod R_q (a request's q sent
+    once for all its chunks).  Bit-identical to the same q replicated per job,
+    and equal to the oracle on the replicated q."""
+    print(f"case: shared q rows {mode} splits={n_splits}", flush=True)
+    Rq, R = 2, 8
+    w = W.random_case(120, R=R, Mq=2, H=16, P=30, NB=10, K=150 if mode == "tokens" else 6,
+                      tokens=mode == "tokens", per_row=mode == "per_row")
+    w.q_lat = np.ascontiguousarray(np.tile(w.q_lat[:Rq], (R // Rq, 1, 1, 1)))
+    w.q_pe = np.ascontiguousarray(np.tile(w.q_pe[:Rq], (R // Rq, 1, 1, 1)))
+    t = G.upload(w)
+    full = mla.sparse_partial_attn(t["q_lat"], t["q_pe"], t["ckv"], t["kpe"], t["table"], t["sel"],
+                                   w.scale, n_splits=n_splits, tokens=w.tokens)
+    shared = mla.sparse_partial_attn(t["q_lat"][:Rq], t["q_pe"][:Rq], t["ckv"], t["kpe"],
+                                     t["table"], t["sel"], w.scale, n_splits=n_splits,
+                                     tokens=w.tokens)
+    torch.cuda.synchronize()
+    assert torch.equal(full[0], shared[0]) and torch.equal(full[1], shared[1])
+    ref_o, ref_l = oracle.partial(w.q_lat, w.q_pe, w.ckv, w.kpe, w.table, w.sel, w.scale,
+                                  tokens=w.tokens)
+    G.assert_parity(shared[0].cpu().numpy().astype(np.float64),
+                    shared[1].cpu().numpy().astype(np.float64), ref_o, ref_l,
+                    f"shared q {mode} splits={n_splits}")
+
+
+def test_shared_q_rows_must_divide_the_jobs():
+    print("case: shared q rows that do not divide R", flush=True)
+    w = W.random_case(121, R=6, Mq=1, H=16, P=10, NB=5, K=3)
+    t = G.upload(w)
+    for rq in (4, 5):
+        with pytest.raises(mla.MlaError) as e:
+            mla.sparse_partial_attn(t["q_lat"][:rq], t["q_pe"][:rq], t["ckv"], t["kpe"], t["table"],
+                                    t["sel"], w.scale)
+        assert e.value.status == mla.MLA_ERR_INVALID_ARGUMENT and "divide" in str(e.value)
